@@ -1,0 +1,126 @@
+"""Seeded synthetic inputs for RIS sparse attention.
+
+This module only *makes inputs*: Gaussian Q/K/V at the layer shapes of the
+paper's host models, the bf16 rounding of those inputs, and the planted
+"needle" similarities of the Structural workload.  It holds none of the
+method's arithmetic (no hash, draw, RoPE or softmax) and is the only code that
+both the CPU oracle's tests and the GPU path's tests use.
+
+The paper evaluates on concatenated scientific manuscripts and QA sets with
+trained Qwen2-1.5B / TinyLlama-1.1B weights; none of those are available, so
+Gaussian activations of the same shapes stand in for them (Results,
+"Empirical Evaluation"; Discussion, "Hardware Context").
+"""
+
+from dataclasses import dataclass, replace
+
+import numpy as np
+
+STOCHASTIC, STRUCTURAL = 0, 1
+ROPE_NONE, ROPE_PLAIN, ROPE_LINEAR, ROPE_YARN = -1, 0, 1, 2
+
+
+@dataclass(frozen=True)
+class Workload:
+    name: str
+    Hq: int
+    Hkv: int
+    D: int
+    N: int
+    dtype: str                 # "f32" or "bf16" (input element type)
+    mode: int
+    density_ppm: int
+    n_seeds: int
+    block: int = 0             # Structural block size (0 = paper rule)
+    rope: int = ROPE_NONE
+    rope_base: float = 10000.0
+    rope_orig: int = 0         # native positional limit
+    rope_factor: float = 0.0   # 0 = window / native limit
+    layers: int = 1
+    needles: bool = False
+    seed: int = 0              # first ensemble seed
+
+    def scaled(self, N):
+        return replace(self, N=N)
+
+
+# The five workloads: a tiny fp32 case, Qwen2-1.5B-shaped layers (12 query /
+# 2 KV heads, head_dim 128) at 32k and 64k tokens, and a TinyLlama-1.1B-shaped
+# layer (32 / 4 heads, head_dim 64) at 64k tokens over 22 layers.
+WORKLOADS = {
+    "tiny": Workload("tiny", 1, 1, 64, 512, "f32", STOCHASTIC, 100_000, 1),
+    "qwen2_32k_stochastic": Workload(
+        "qwen2_32k_stochastic", 12, 2, 128, 32768, "bf16", STOCHASTIC, 10_000, 10,
+        rope=ROPE_PLAIN, rope_base=1e6, rope_orig=32768),
+    "qwen2_32k_structural": Workload(
+        "qwen2_32k_structural", 12, 2, 128, 32768, "bf16", STRUCTURAL, 10_000, 10,
+        block=64, rope=ROPE_PLAIN, rope_base=1e6, rope_orig=32768, needles=True),
+    "qwen2_64k_stochastic_yarn": Workload(
+        "qwen2_64k_stochastic_yarn", 12, 2, 128, 65536, "bf16", STOCHASTIC, 10_000, 70,
+        rope=ROPE_YARN, rope_base=1e6, rope_orig=32768),
+    "tinyllama_64k_structural": Workload(
+        "tinyllama_64k_structural", 32, 4, 64, 65536, "bf16", STRUCTURAL, 50_000, 10,
+        block=64, layers=22),
+}
+
+
+def gaussian_qkv(Hq, Hkv, N, D, seed=0):
+    """Q [Hq,N,D], K [Hkv,N,D], V [Hkv,N,D] ~ N(0,1) float32, drawn in that
+    order from ``numpy.random.default_rng(seed)``."""
+    rng = np.random.default_rng(seed)
+    Q = rng.standard_normal((Hq, N, D), dtype=np.float32)
+    K = rng.standard_normal((Hkv, N, D), dtype=np.float32)
+    V = rng.standard_normal((Hkv, N, D), dtype=np.float32)
+    return Q, K, V
+
+
+def to_bf16(x):
+    """Round a float32 array to bfloat16 (round to nearest even).
+
+    Returns a torch.bfloat16 CPU tensor; ``.float().numpy()`` gives the exact
+    values it holds.
+    """
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32)).to(torch.bfloat16)
+
+
+def needle_plan(N, seed=1, span=512, per_span=8, targets=64):
+    """Needle positions and their target queries.
+
+    In every ``span``-token window ``per_span`` key positions p are chosen;
+    for each p, ``targets`` query rows are chosen uniformly without
+    replacement from [p, N) (all of them if fewer remain).  Returns arrays
+    (p, i) of equal length.
+    """
+    rng = np.random.default_rng(seed)
+    ps, iss = [], []
+    for s0 in range(0, N, span):
+        width = min(span, N - s0)
+        pos = s0 + rng.choice(width, size=min(per_span, width), replace=False)
+        for p in np.sort(pos):
+            avail = N - p
+            t = rng.choice(avail, size=min(targets, avail), replace=False) + p
+            ps.append(np.full(t.shape, p, dtype=np.int64))
+            iss.append(t.astype(np.int64))
+    return np.concatenate(ps), np.concatenate(iss)
+
+
+def plant_needles(Q, K, plan, sigma_mult=3.0):
+    """Raise <Q[h,i], K[g,p]> by sigma_mult * sqrt(D) for every planned (p, i)
+    and every query head h of KV group g.
+
+    Q: [Hq,N,D] float array (modified copy returned), K: [Hkv,N,D].  Applied
+    to rotated (post-RoPE) vectors, so the logit gain is exact.
+    """
+    Q = np.array(Q, dtype=np.float64, copy=True)
+    K = np.asarray(K, dtype=np.float64)
+    Hq, N, D = Q.shape
+    Hkv = K.shape[0]
+    G = Hq // Hkv
+    p, i = plan
+    for g in range(Hkv):
+        kp = K[g, p]                                          # [P, D]
+        add = sigma_mult * np.sqrt(D) * kp / np.sum(kp * kp, axis=1, keepdims=True)
+        for h in range(g * G, (g + 1) * G):
+            np.add.at(Q[h], i, add)
+    return Q
