@@ -1,0 +1,227 @@
+"""Benchmark of the RIS sparse-attention hot path on one MI355X.
+
+One step = one layer of the hot path over resident synthetic inputs:
+restore Q and K from pristine copies (RoPE rotates in place), RoPE on Q and K,
+geometry (count pass, scan, fill pass of the CSR), sparse attention.  The
+default workload is the Qwen2-1.5B-shaped layer at N = 65,536 tokens, 1%
+density, 70 seeds, YaRN x2 -- the configuration the headline metric names.
+
+Prints ONE JSON line (see the fields below).  `value` is attended
+(query-head, key) pairs per second of whole step time.
+"""
+import argparse
+import json
+import multiprocessing as mp
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+from synth import ROPE_NONE, STRUCTURAL, WORKLOADS, gaussian_qkv, needle_plan, plant_needles  # noqa: E402
+
+HBM_PEAK_GBS = 8000.0
+KV_PAIR_BYTES = {128: 2 * 128 * 2 + 4, 64: 2 * 64 * 2 + 4}   # K row + V row (bf16) + int32 index
+
+
+# ---------------------------------------------------------------------------
+# CPU baseline: the oracle as it stands, on a bounded row sample.
+# ---------------------------------------------------------------------------
+_CPU = {}
+
+
+def _cpu_init(state):
+    # One BLAS thread per worker process: oversubscribed BLAS threads saturate
+    # the memory bus (the paper's thread-count lesson).
+    from threadpoolctl import threadpool_limits
+    _CPU["limits"] = threadpool_limits(1)
+    _CPU.update(state)
+
+
+def _cpu_rows(task):
+    from oracle import attention as o_att
+    from oracle import geometry as o_geo
+    s = _CPU
+    sp, G, D = s["spec"], s["G"], s["D"]
+    g, qs = task
+    t0 = time.perf_counter()
+    sets = o_geo.row_sets(sp, g, np.asarray(qs))
+    pairs = 0
+    for q, I in zip(qs, sets):
+        Ksel, Vsel = s["Kr"][g, I], s["V"][g, I]      # one gather serves the G heads
+        for hh in range(G):
+            o_att.attend_one(s["Qr"][g * G + hh, q], Ksel, Vsel, 1 / np.sqrt(D))
+            pairs += len(I)
+    return pairs, time.perf_counter() - t0
+
+
+def cpu_baseline(w, layer, Q, K, V, workers, stride):
+    """Oracle pairs/s over every `stride`-th query row of each KV head."""
+    from oracle import geometry as o_geo
+    from oracle import rope as o_rope
+    t_rope = 0.0
+    qs = np.arange(stride - 1, w.N, stride)
+    Qr, Kr = Q, K
+    if w.rope != ROPE_NONE:
+        s = o_rope.scale_factor(w.rope_factor, w.N, w.rope_orig) if w.rope != o_rope.PLAIN else 1.0
+        t0 = time.perf_counter()
+        Kr = o_rope.apply(K, w.rope, w.rope_base, 0, s, w.rope_orig)
+        Qr = np.zeros_like(Q)
+        Qr[:, qs] = o_rope.apply(Q[:, qs], w.rope, w.rope_base, 0, s, w.rope_orig, positions=qs)
+        # K is rotated once for all rows; charge the sample its share of it.
+        t_rope = (time.perf_counter() - t0) * (len(qs) / w.N)
+    spec = o_geo.MaskSpec(mode=w.mode, density_ppm=w.density_ppm, seed=w.seed,
+                          n_seeds=w.n_seeds, layer=layer, N=w.N, heads=w.Hkv, block=w.block)
+    state = dict(spec=spec, G=w.Hq // w.Hkv, D=w.D, Qr=Qr, Kr=Kr, V=V)
+    # Heavy rows (large q) first, interleaved over tasks of 8 rows.
+    tasks = [(g, list(qs[::-1][i:i + 8])) for g in range(w.Hkv) for i in range(0, len(qs), 8)]
+    ctx = mp.get_context("fork")
+    t0 = time.perf_counter()
+    with ctx.Pool(workers, initializer=_cpu_init, initargs=(state,)) as pool:
+        res = pool.map(_cpu_rows, tasks, chunksize=1)
+    wall = time.perf_counter() - t0 + t_rope
+    pairs = sum(r[0] for r in res)
+    return {"value": pairs / wall, "unit": "pairs/s", "cores": workers, "kind": "oracle",
+            "sample": f"every {stride}th query row of each KV head ({len(qs) * w.Hkv} rows, "
+                      f"{pairs} attended pairs), geometry + RoPE share + attention, "
+                      f"{wall:.1f} s wall on {workers} worker processes"}
+
+
+# ---------------------------------------------------------------------------
+# GPU
+# ---------------------------------------------------------------------------
+def run_gpu(w, layer, Q, K, V, steps, warmup, algo):
+    import torch
+    from paper_2607_21927_amd import ris
+    from synth import to_bf16
+    dev = torch.device("cuda:0")
+    q0, k0, v = to_bf16(Q).to(dev), to_bf16(K).to(dev), to_bf16(V).to(dev)
+    if w.needles:
+        # Needles are planted on rotated vectors; this workload's step then
+        # starts from the rotated, planted inputs and skips RoPE.
+        raise SystemExit("needle workload: run its parity test instead")
+    q, k = torch.empty_like(q0), torch.empty_like(k0)
+    out = torch.empty(w.Hq, w.N, w.D, dtype=torch.bfloat16, device=dev)
+    desc = ris.mask_desc(w.mode, w.density_ppm, w.N, w.Hkv, n_seeds=w.n_seeds, seed=w.seed,
+                         layer=layer, block=w.block)
+    cap = ris.mask_nnz_bound(desc)
+    row_ptr = torch.empty(w.Hkv * w.N + 1, dtype=torch.int64, device=dev)
+    col_idx = torch.empty(cap, dtype=torch.int32, device=dev)
+    rd = (ris.rope_desc(w.rope, w.rope_base, orig_max_pos=w.rope_orig, factor=w.rope_factor)
+          if w.rope != ROPE_NONE else None)
+    ad = ris.attn_desc(q, k, out, mode=w.mode, block=w.block, algo=algo)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(5)]
+
+    def step(record):
+        q.copy_(q0)
+        k.copy_(k0)
+        if record:
+            ev[0].record()
+        if rd is not None:
+            ris.rope(q, rd)
+            ris.rope(k, rd)
+        if record:
+            ev[1].record()
+        ris.mask_build(desc, row_ptr)
+        ris.mask_build(desc, row_ptr, col_idx, col_capacity=cap)
+        if record:
+            ev[2].record()
+        ris.sparse_attn(q, k, v, row_ptr, col_idx, out, ad)
+        if record:
+            ev[3].record()
+
+    for _ in range(warmup):
+        step(False)
+    torch.cuda.synchronize()
+    t_rope = t_mask = t_attn = 0.0
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    per_step = []
+    for _ in range(steps):
+        step(True)
+        per_step.append(tuple(ev[:4]))
+        # Fresh events for the next step so every step's stamps survive.
+        ev[:4] = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+    end.record()
+    torch.cuda.synchronize()
+    total_ms = start.elapsed_time(end)
+    for e0, e1, e2, e3 in per_step:
+        t_rope += e0.elapsed_time(e1)
+        t_mask += e1.elapsed_time(e2)
+        t_attn += e2.elapsed_time(e3)
+    nnz = int(row_ptr[-1].item())
+    return dict(ms_step=total_ms / steps, ms_rope=t_rope / steps, ms_mask=t_mask / steps,
+                ms_attn=t_attn / steps, nnz=nnz)
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="qwen2_64k_stochastic_yarn", choices=sorted(WORKLOADS))
+    ap.add_argument("--layer", type=int, default=0)
+    ap.add_argument("--algo", type=int, default=0, help="0 auto, 1 gather, 2 tile")
+    ap.add_argument("--cpu-workers", type=int, default=16)
+    ap.add_argument("--cpu-stride", type=int, default=64)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU only: the hot path needs no cross-GPU exchange and this "
+              "build has no multi-GPU launch (run with --gpus 1).", file=sys.stderr)
+        sys.exit(2)
+    w = WORKLOADS[args.workload]
+    Q, K, V = gaussian_qkv(w.Hq, w.Hkv, w.N, w.D, seed=0)
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        # Before any GPU call: the worker pool forks this process.
+        workers = max(1, min(args.cpu_workers, os.cpu_count() or 1))
+        from synth import to_bf16
+        Qb, Kb, Vb = (to_bf16(x).float().numpy() for x in (Q, K, V))
+        cpu = cpu_baseline(w, args.layer, Qb, Kb, Vb, workers, args.cpu_stride)
+        del Qb, Kb, Vb
+
+    g = run_gpu(w, args.layer, Q, K, V, args.steps, args.warmup, args.algo)
+    G = w.Hq // w.Hkv
+    pairs = g["nnz"] * G
+    causal_pairs = w.Hkv * w.N * (w.N + 1) / 2
+    alg_bytes = g["nnz"] * KV_PAIR_BYTES[w.D]
+    achieved = alg_bytes / (g["ms_attn"] * 1e-3) / 1e9
+    res = {
+        "metric": "attended (q,k) pairs/s (whole hot-path step: RoPE + geometry + attention)",
+        "value": pairs / (g["ms_step"] * 1e-3),
+        "unit": "pairs/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": g["ms_step"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic: Gaussian Q/K/V (numpy default_rng(0)) at the layer shape",
+        "config": {"workload": w.name, "Hq": w.Hq, "Hkv": w.Hkv, "head_dim": w.D, "N": w.N,
+                   "mode": "structural" if w.mode == STRUCTURAL else "stochastic",
+                   "density": w.density_ppm / 1e6, "seeds": w.n_seeds, "block": w.block,
+                   "rope": ["none", "plain", "linear", "yarn"][w.rope + 1], "layer": args.layer},
+        "ms_per_layer_attn": g["ms_attn"],
+        "ms_geometry": g["ms_mask"],
+        "ms_rope": g["ms_rope"],
+        "attn_pairs_per_s": pairs / (g["ms_attn"] * 1e-3),
+        "kv_pairs": g["nnz"],
+        "union_fraction": g["nnz"] / causal_pairs,
+        "hbm_gbs_attn": achieved,
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "kernel": "sparse attention", "bytes_per_kv_pair": KV_PAIR_BYTES[w.D]},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(res))
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,194 @@
+/*
+ * ris.h -- C ABI of the RIS sparse-attention library for AMD Instinct MI355X
+ * (gfx950).  Plain C types only: device pointers, sizes and small descriptor
+ * structs.  Every call is asynchronous on the given HIP stream (a
+ * hipStream_t passed as void*, NULL = the default stream) unless its comment
+ * says otherwise.
+ *
+ * Errors: every call returns RIS_OK (0) or a negative ris_status.  Arguments
+ * are validated on the host before anything is launched; a call that fails
+ * validation launches nothing and writes nothing.  A HIP runtime failure maps
+ * to RIS_E_HIP.  Nothing aborts and no exception crosses the ABI.
+ *
+ * Ownership: the caller allocates every buffer; the library keeps no global
+ * mutable state and no allocation alive between calls.
+ *
+ * The operations follow the paper "RIS-Kernel: A Model-Agnostic Architecture
+ * for Long-Context LLM Inference via Sparse Attention": geometry generation
+ * (Methods, "Memory-Bounded Geometry Generation" and "Sampling Modes"),
+ * RoPE scaling (Methods, "Dynamic RoPE Scaling") and one softmax over the
+ * unified index set (Methods, "Hybrid Anchor and Pre-Fusion Unified
+ * Softmax").
+ */
+#ifndef RIS_H
+#define RIS_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    RIS_OK = 0,
+    RIS_E_ARG = -1,          /* null pointer or out-of-range scalar          */
+    RIS_E_SHAPE = -2,        /* inconsistent sizes (e.g. Hq % Hkv != 0)      */
+    RIS_E_DTYPE = -3,        /* unknown element type                         */
+    RIS_E_CAPACITY = -4,     /* col_idx capacity below the number of entries */
+    RIS_E_UNSUPPORTED = -5,  /* valid request outside what is implemented    */
+    RIS_E_HIP = -6           /* HIP runtime error                            */
+} ris_status;
+
+typedef enum { RIS_STOCHASTIC = 0, RIS_STRUCTURAL = 1 } ris_mode;
+typedef enum { RIS_F32 = 0, RIS_BF16 = 1 } ris_dtype;
+typedef enum { RIS_ROPE_PLAIN = 0, RIS_ROPE_LINEAR = 1, RIS_ROPE_YARN = 2 } ris_rope_kind;
+typedef enum { RIS_ATTN_AUTO = 0, RIS_ATTN_GATHER = 1, RIS_ATTN_TILE = 2 } ris_attn_algo;
+
+/* Largest sequence length the geometry kernels accept (one row's pool is a
+ * bitmap in on-chip LDS). */
+#define RIS_MAX_N 262144
+/* Largest ensemble size per call. */
+#define RIS_MAX_SEEDS 4096
+
+/* ------------------------------------------------------------------------ */
+/* Geometry: per-query key sets as CSR                                       */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * What one layer's geometry depends on.
+ *
+ * Row r = kv_head * N + q holds I(kv_head, q), the union over the seeds
+ * seed, seed+1, ..., seed+n_seeds-1 of each seed's set, ascending and without
+ * duplicates (the seeds merge into one master set; Methods, "Memory-Bounded
+ * Geometry Generation"; ensemble union, Results, "Ensemble Coverage
+ * Analysis").
+ *
+ * Per seed, with pool size n_q = q+1 (causal) or N, the row draws exactly
+ *   k(q) = clamp(floor((density_ppm * n_q + 500000) / 1000000), 1, n_q)
+ * distinct keys, uniformly (Methods, "Sampling Modes", Stochastic).  In
+ * Structural mode the row holds its block clique [bB, q] (b = floor(q/B)) plus
+ * k_g = min(bB, max(0, k(q) - (q - bB + 1))) keys drawn uniformly from
+ * [0, bB): the clique's cost is deducted from the global budget (Methods,
+ * "Sampling Modes", Structural).  The draw of seed s for row (layer, kv_head,
+ * q) is a keyed Feistel permutation of the pool whose six round keys are the
+ * first six 32-bit words of Philox4x64-10(counter = (q, kv_head, layer, 0),
+ * key = (s, 0)); a keyed permutation yields distinct keys with no dedupe.
+ */
+typedef struct {
+    int32_t  mode;          /* ris_mode                                        */
+    int32_t  density_ppm;   /* density d in parts per million, 1..1000000      */
+    uint64_t seed;          /* first ensemble seed                             */
+    int32_t  n_seeds;       /* S, 1..RIS_MAX_SEEDS                             */
+    int32_t  layer;         /* layer index (>= 0), enters the hash             */
+    int64_t  N;             /* sequence length, 1..RIS_MAX_N                   */
+    int32_t  heads;         /* KV heads (>= 1); query heads of a group share   */
+    int32_t  causal;        /* 1 = pool [0, q]; 0 = pool [0, N) (Stochastic)   */
+    int32_t  block;         /* Structural block B; 0 = min(N/10, B_max) with   */
+                            /* B_max = k evaluated on n = N                    */
+} ris_mask_desc;
+
+/*
+ * Build the CSR of one layer's geometry, in two phases.
+ *
+ * row_ptr: device int64[heads*N + 1].  col_idx: device int32[col_capacity].
+ *
+ * Count phase (col_idx == NULL): writes row_ptr, the exclusive prefix sum of
+ *   the row sizes (row_ptr[0] = 0, row_ptr[heads*N] = nnz).  The caller then
+ *   reads row_ptr[heads*N] (8 bytes) to size col_idx, or sizes it with
+ *   ris_mask_nnz_bound() and skips that read.
+ * Fill phase (col_idx != NULL): row_ptr must hold the count phase's output
+ *   for the same descriptor; writes col_idx[row_ptr[r] .. row_ptr[r+1]) for
+ *   every row.  If col_capacity >= ris_mask_nnz_bound(desc) the call is fully
+ *   asynchronous; otherwise it first reads row_ptr[heads*N] (synchronising
+ *   the stream) and returns RIS_E_CAPACITY, writing nothing, when
+ *   col_capacity < nnz.  Writes never leave col_idx[0 .. col_capacity).
+ * Requires Structural mode to be causal.
+ */
+int ris_mask_build(const ris_mask_desc* desc, int64_t* row_ptr, int32_t* col_idx,
+                   int64_t col_capacity, void* stream);
+
+/*
+ * Host-only closed-form upper bound on nnz for the descriptor:
+ * sum over rows of min(pool, n_seeds * draws) (+ clique), times heads.
+ * Exact when n_seeds == 1.  Returns a negative ris_status on a bad descriptor.
+ */
+int64_t ris_mask_nnz_bound(const ris_mask_desc* desc);
+
+/* ------------------------------------------------------------------------ */
+/* RoPE with the paper's long-context scaling                               */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * Scaling of the rotary frequencies (Methods, "Dynamic RoPE Scaling"; Results,
+ * "Linear Interpolation" and "YaRN").  The factor is requested window /
+ * native limit; the frequencies are those of the Hugging Face configuration
+ * pathway the paper hooks:
+ *   plain:  f_i = base^(-2i/D)
+ *   linear: f_i / s
+ *   YaRN:   ramp t_i = clamp((i - lo) / (hi - lo), 0, 1) with
+ *           lo = max(floor(c(beta_fast)), 0), hi = min(ceil(c(beta_slow)), D-1),
+ *           c(r) = D ln(orig_max_pos / (2 pi r)) / (2 ln base);
+ *           f'_i = t_i f_i / s + (1 - t_i) f_i;  cos, sin scaled by
+ *           0.1 ln s + 1 when s > 1.
+ */
+typedef struct {
+    int32_t kind;            /* ris_rope_kind                                  */
+    double  base;            /* rotary base (theta), > 1                       */
+    int64_t orig_max_pos;    /* native positional limit (linear/YaRN), > 0     */
+    double  factor;          /* s; 0 = max(1, (pos0 + N) / orig_max_pos)       */
+    double  beta_slow;       /* YaRN; 0 = 1                                    */
+    double  beta_fast;       /* YaRN; 0 = 32                                   */
+} ris_rope_desc;
+
+/*
+ * Rotate x in place: x is device [heads, N, D] contiguous, element type dtype
+ * (ris_dtype).  Token t has position pos0 + t.  Dimension i pairs with
+ * i + D/2: y_i = x_i c - x_{i+D/2} s, y_{i+D/2} = x_{i+D/2} c + x_i s, with the
+ * angle (pos0 + t) f'_i evaluated in float64, c and s (times the YaRN factor)
+ * rounded to float32, the rotation in float32, and bf16 results rounded to
+ * nearest even.  D must be even, 2..512.
+ */
+int ris_rope(void* x, int32_t dtype, int32_t heads, int64_t N, int32_t D, int64_t pos0,
+             const ris_rope_desc* desc, void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* Sparse attention over the unified index sets                             */
+/* ------------------------------------------------------------------------ */
+
+typedef struct {
+    int32_t dtype_in;        /* ris_dtype of Q, K, V                            */
+    int32_t dtype_out;       /* ris_dtype of out                                */
+    int32_t Hq;              /* query heads                                     */
+    int32_t Hkv;             /* KV heads; Hq % Hkv == 0, G = Hq / Hkv <= 8       */
+    int64_t N;               /* sequence length                                 */
+    int32_t D;               /* head dimension: 64 or 128                       */
+    float   scale;           /* score scale; 0 = 1 / sqrt(D)                    */
+    int32_t mode;            /* ris_mode the CSR was built with                 */
+    int32_t block;           /* its Structural block (as in ris_mask_desc)      */
+    int32_t causal;          /* as in ris_mask_desc                             */
+    int32_t algo;            /* ris_attn_algo; AUTO picks per tile              */
+} ris_attn_desc;
+
+/*
+ * out[h, q, :] = sum_{j in I(g, q)} softmax_j(scale <Q[h,q], K[g,j]>) V[g, j]
+ * with g = floor(h / G): one normalisation over the whole unified set of the
+ * row, every index once (Pre-Fusion Unified Softmax; Methods, "Hybrid Anchor
+ * and Pre-Fusion Unified Softmax").  Q, out: device [Hq, N, D]; K, V: device
+ * [Hkv, N, D]; contiguous.  row_ptr / col_idx: the CSR from ris_mask_build
+ * with heads = Hkv and the same N (ascending rows, entries in [0, N)).
+ * Accumulation is float32.  An empty row yields zeros.
+ */
+int ris_sparse_attn(const void* Q, const void* K, const void* V, const int64_t* row_ptr,
+                    const int32_t* col_idx, void* out, const ris_attn_desc* desc, void* stream);
+
+/* Human-readable name of a ris_status (static string, never NULL). */
+const char* ris_status_string(int status);
+
+/* Library ABI version: (major << 16) | minor. */
+int ris_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RIS_H */

@@ -79,10 +79,15 @@ def cos_sin(kind, D, base, positions, s=1.0, orig_max_pos=None, beta_slow=1.0, b
     return np.cos(ang) * ms, np.sin(ang) * ms
 
 
-def apply(x, kind, base, pos0=0, s=1.0, orig_max_pos=None, beta_slow=1.0, beta_fast=32.0):
-    """Rotate x [heads, N, D] (any float dtype) in float64; returns float64."""
+def apply(x, kind, base, pos0=0, s=1.0, orig_max_pos=None, beta_slow=1.0, beta_fast=32.0,
+          positions=None):
+    """Rotate x [heads, N, D] (any float dtype) in float64; returns float64.
+
+    Token t sits at position pos0 + t, or at positions[t] when given.
+    """
     x = np.asarray(x, dtype=np.float64)
     H, N, D = x.shape
-    c, sn = cos_sin(kind, D, base, np.arange(pos0, pos0 + N), s, orig_max_pos, beta_slow, beta_fast)
+    pos = np.arange(pos0, pos0 + N) if positions is None else np.asarray(positions)
+    c, sn = cos_sin(kind, D, base, pos, s, orig_max_pos, beta_slow, beta_fast)
     x1, x2 = x[..., : D // 2], x[..., D // 2:]
     return np.concatenate([x1 * c - x2 * sn, x2 * c + x1 * sn], axis=-1)

@@ -1,0 +1,246 @@
+// Geometry kernels: per-row key sets of the seed ensemble, emitted as CSR.
+//
+// One workgroup builds one row (kv_head, q).  The row's pool is a bitmap in
+// LDS; every (seed, draw) pair of the ensemble is spread over the 256 lanes,
+// each lane evaluates the keyed permutation and ORs its key into the bitmap.
+// The bitmap *is* the union over seeds (the paper merges every seed into one
+// master set and discards the seed; Methods, "Memory-Bounded Geometry
+// Generation"), and reading it in word order yields the row ascending and
+// without duplicates (the unique() merge; Methods, "Hybrid Anchor and
+// Pre-Fusion Unified Softmax").
+//
+// Count pass: popcount -> row size -> row_ptr[r + 1]; a single-workgroup
+// scan turns sizes into offsets.  Fill pass: regenerate the bitmap, then a
+// block-wide prefix over word popcounts places every key.  Rows are launched
+// in descending q (their cost grows with q) so the heavy rows start first.
+#include "ris_device.h"
+#include "ris_internal.h"
+
+namespace ris {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kSeedBatch = 64;   // round keys of this many seeds live in LDS at once
+
+struct RowGeom {
+    uint32_t pool;          // draw pool [0, pool)
+    uint32_t draws;         // keys per seed
+    uint32_t clique_start;  // Structural clique [clique_start, q]
+    uint32_t clique_len;
+};
+
+__device__ __forceinline__ RowGeom row_geometry(const MaskParams& p, int64_t q) {
+    RowGeom g;
+    if (p.mode == 0) {
+        const int64_t n = p.causal ? q + 1 : p.N;
+        g.pool = (uint32_t)n;
+        g.draws = (uint32_t)row_count(p.ppm, n);
+        g.clique_start = 0;
+        g.clique_len = 0;
+    } else {
+        const int64_t start = (q / p.block) * (int64_t)p.block;
+        const int64_t clique = q - start + 1;
+        const int64_t k = row_count(p.ppm, q + 1);
+        int64_t kg = k - clique;
+        if (kg < 0) kg = 0;
+        if (kg > start) kg = start;
+        g.pool = (uint32_t)start;
+        g.draws = (uint32_t)kg;
+        g.clique_start = (uint32_t)start;
+        g.clique_len = (uint32_t)clique;
+    }
+    return g;
+}
+
+// Fill `bits` (W words, already visible to the whole block) with the union of
+// every seed's draws for row (h, q).  Ends with a block barrier.
+__device__ void build_row_bitmap(const MaskParams& p, int64_t q, int h, const RowGeom& g,
+                                 uint32_t* rks, uint32_t* bits) {
+    const int tid = threadIdx.x;
+    const uint32_t W = (g.pool + 31u) >> 5;
+    for (uint32_t w = tid; w < W; w += kThreads) bits[w] = 0u;
+    if (g.draws == 0) {
+        __syncthreads();
+        return;
+    }
+    const FeistelDomain dom = make_domain(g.pool);
+    const float inv_draws = 1.0f / (float)g.draws;
+    for (int s0 = 0; s0 < p.n_seeds; s0 += kSeedBatch) {
+        const int sb = min(kSeedBatch, p.n_seeds - s0);
+        __syncthreads();   // bitmap cleared / previous batch's keys no longer read
+        for (int t = tid; t < sb; t += kThreads) {
+            uint32_t rk[6];
+            row_round_keys(p.seed + (uint64_t)(s0 + t), (uint64_t)q, (uint64_t)h, (uint64_t)p.layer, rk);
+#pragma unroll
+            for (int e = 0; e < 6; ++e) rks[t * 6 + e] = rk[e];
+        }
+        __syncthreads();
+        const uint32_t total = (uint32_t)sb * g.draws;   // < 2^24: float index math is exact
+        for (uint32_t idx = tid; idx < total; idx += kThreads) {
+            int s = (int)((float)idx * inv_draws);
+            int j = (int)idx - s * (int)g.draws;
+            if (j < 0) { --s; j += (int)g.draws; }
+            if (j >= (int)g.draws) { ++s; j -= (int)g.draws; }
+            uint32_t rk[6];
+#pragma unroll
+            for (int e = 0; e < 6; ++e) rk[e] = rks[s * 6 + e];
+            const uint32_t x = permute((uint32_t)j, rk, dom);
+            atomicOr(&bits[x >> 5], 1u << (x & 31u));
+        }
+    }
+    __syncthreads();
+}
+
+__device__ __forceinline__ uint32_t block_sum(uint32_t v, uint32_t* red) {
+    const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+    v = wave_sum_u32(v);
+    if (lane == 0) red[wid] = v;
+    __syncthreads();
+    const uint32_t t = red[0] + red[1] + red[2] + red[3];
+    __syncthreads();
+    return t;
+}
+
+// Exclusive prefix of v over the block; *total receives the block sum.
+__device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* red, uint32_t* total) {
+    const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+    const uint32_t inc = wave_inclusive_scan(v, lane);
+    if (lane == 63) red[wid] = inc;
+    __syncthreads();
+    uint32_t before = 0;
+    for (int w = 0; w < wid; ++w) before += red[w];
+    *total = red[0] + red[1] + red[2] + red[3];
+    __syncthreads();
+    return before + inc - v;
+}
+
+__device__ __forceinline__ void row_of_block(const MaskParams& p, int64_t& q, int& h) {
+    const int64_t i = blockIdx.x;
+    q = p.N - 1 - i / p.heads;
+    h = (int)(i % p.heads);
+}
+
+__global__ __launch_bounds__(kThreads) void k_mask_count(MaskParams p, int64_t* row_ptr) {
+    extern __shared__ uint32_t smem[];
+    __shared__ uint32_t red[4];
+    uint32_t* rks = smem;
+    uint32_t* bits = smem + kSeedBatch * 6;
+    int64_t q; int h;
+    row_of_block(p, q, h);
+    const RowGeom g = row_geometry(p, q);
+    build_row_bitmap(p, q, h, g, rks, bits);
+    const uint32_t W = (g.pool + 31u) >> 5;
+    uint32_t c = 0;
+    for (uint32_t w = threadIdx.x; w < W; w += kThreads) c += __popc(bits[w]);
+    const uint32_t total = block_sum(c, red);
+    if (threadIdx.x == 0) row_ptr[(int64_t)h * p.N + q + 1] = (int64_t)total + g.clique_len;
+}
+
+__global__ __launch_bounds__(kThreads) void k_mask_fill(MaskParams p, const int64_t* row_ptr,
+                                                        int32_t* col_idx, int64_t capacity) {
+    extern __shared__ uint32_t smem[];
+    __shared__ uint32_t red[4];
+    uint32_t* rks = smem;
+    uint32_t* bits = smem + kSeedBatch * 6;
+    int64_t q; int h;
+    row_of_block(p, q, h);
+    const int64_t r = (int64_t)h * p.N + q;
+    const int64_t base = row_ptr[r];
+    int64_t limit = row_ptr[r + 1] - base;
+    // Never write outside col_idx[0, capacity), whatever row_ptr holds.
+    if (base < 0 || limit < 0 || base > capacity) return;
+    if (limit > capacity - base) limit = capacity - base;
+    const RowGeom g = row_geometry(p, q);
+    build_row_bitmap(p, q, h, g, rks, bits);
+    const uint32_t W = (g.pool + 31u) >> 5;
+    int32_t* out = col_idx + base;
+    uint32_t done = 0;
+    for (uint32_t w0 = 0; w0 < W; w0 += kThreads) {
+        const uint32_t w = w0 + threadIdx.x;
+        uint32_t word = w < W ? bits[w] : 0u;
+        uint32_t total;
+        int64_t pos = done + block_exclusive_scan(__popc(word), red, &total);
+        while (word) {
+            const uint32_t b = __ffs(word) - 1u;
+            word &= word - 1u;
+            if (pos < limit) out[pos] = (int32_t)(w * 32u + b);
+            ++pos;
+        }
+        done += total;
+    }
+    for (uint32_t t = threadIdx.x; t < g.clique_len; t += kThreads) {
+        const int64_t pos = (int64_t)done + t;
+        if (pos < limit) out[pos] = (int32_t)(g.clique_start + t);
+    }
+}
+
+// In-place inclusive scan of row_ptr[1 .. R] (row sizes -> end offsets);
+// row_ptr[0] = 0.  One workgroup walks the array in coalesced chunks.
+constexpr int kScanThreads = 1024;
+constexpr int kScanItems = 4;
+
+__global__ __launch_bounds__(kScanThreads) void k_scan_rows(int64_t* row_ptr, int64_t R) {
+    __shared__ int64_t wave_tot[kScanThreads / 64];
+    const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+    int64_t carry = 0;
+    if (tid == 0) row_ptr[0] = 0;
+    for (int64_t base = 1; base <= R; base += (int64_t)kScanThreads * kScanItems) {
+        int64_t v[kScanItems];
+        int64_t run = 0;
+#pragma unroll
+        for (int e = 0; e < kScanItems; ++e) {
+            const int64_t idx = base + (int64_t)tid * kScanItems + e;
+            run += idx <= R ? row_ptr[idx] : 0;
+            v[e] = run;
+        }
+        int64_t inc = run;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+            const int64_t t = __shfl_up(inc, off);
+            if (lane >= off) inc += t;
+        }
+        if (lane == 63) wave_tot[wid] = inc;
+        __syncthreads();
+        int64_t before = carry;
+        int64_t chunk = 0;
+        for (int w = 0; w < kScanThreads / 64; ++w) {
+            if (w < wid) before += wave_tot[w];
+            chunk += wave_tot[w];
+        }
+        before += inc - run;
+#pragma unroll
+        for (int e = 0; e < kScanItems; ++e) {
+            const int64_t idx = base + (int64_t)tid * kScanItems + e;
+            if (idx <= R) row_ptr[idx] = before + v[e];
+        }
+        carry += chunk;
+        __syncthreads();
+    }
+}
+
+size_t mask_smem_bytes(const MaskParams& p) {
+    const int64_t words = (p.N + 31) / 32;
+    return (size_t)(kSeedBatch * 6 + words) * sizeof(uint32_t);
+}
+
+}  // namespace
+
+hipError_t launch_mask_count(const MaskParams& p, int64_t* row_ptr, hipStream_t st) {
+    const int64_t rows = (int64_t)p.heads * p.N;
+    hipLaunchKernelGGL(k_mask_count, dim3((unsigned)rows), dim3(kThreads), mask_smem_bytes(p), st, p,
+                       row_ptr);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_scan_rows, dim3(1), dim3(kScanThreads), 0, st, row_ptr, rows);
+    return hipGetLastError();
+}
+
+hipError_t launch_mask_fill(const MaskParams& p, const int64_t* row_ptr, int32_t* col_idx,
+                            int64_t capacity, hipStream_t st) {
+    const int64_t rows = (int64_t)p.heads * p.N;
+    hipLaunchKernelGGL(k_mask_fill, dim3((unsigned)rows), dim3(kThreads), mask_smem_bytes(p), st, p,
+                       row_ptr, col_idx, capacity);
+    return hipGetLastError();
+}
+
+}  // namespace ris

@@ -1,0 +1,194 @@
+// C ABI of the RIS library: argument validation, parameter resolution and
+// kernel dispatch.  Nothing here allocates device memory or keeps state.
+#include <math.h>
+#include <stdint.h>
+
+#include "ris.h"
+#include "ris_device.h"
+#include "ris_internal.h"
+
+namespace {
+
+using ris::MaskParams;
+
+int validate_mask(const ris_mask_desc* d) {
+    if (!d) return RIS_E_ARG;
+    if (d->mode != RIS_STOCHASTIC && d->mode != RIS_STRUCTURAL) return RIS_E_ARG;
+    if (d->density_ppm < 1 || d->density_ppm > 1000000) return RIS_E_ARG;
+    if (d->n_seeds < 1 || d->n_seeds > RIS_MAX_SEEDS) return RIS_E_ARG;
+    if (d->layer < 0) return RIS_E_ARG;
+    if (d->N < 1 || d->N > RIS_MAX_N) return RIS_E_ARG;
+    if (d->heads < 1 || d->heads > 8192) return RIS_E_ARG;
+    if (d->causal != 0 && d->causal != 1) return RIS_E_ARG;
+    if (d->block < 0) return RIS_E_ARG;
+    if (d->mode == RIS_STRUCTURAL && !d->causal) return RIS_E_UNSUPPORTED;
+    return RIS_OK;
+}
+
+// Structural block size: explicit, or min(floor(N / 10), B_max) with B_max the
+// count rule evaluated on n = N (at least 1).
+int32_t resolve_block(const ris_mask_desc* d) {
+    if (d->mode != RIS_STRUCTURAL) return 1;
+    if (d->block > 0) return d->block;
+    int64_t b = ris::row_count(d->density_ppm, d->N);
+    if (d->N / 10 < b) b = d->N / 10;
+    return b < 1 ? 1 : (int32_t)b;
+}
+
+MaskParams make_params(const ris_mask_desc* d) {
+    MaskParams p;
+    p.seed = d->seed;
+    p.N = d->N;
+    p.mode = d->mode;
+    p.ppm = d->density_ppm;
+    p.n_seeds = d->n_seeds;
+    p.layer = d->layer;
+    p.heads = d->heads;
+    p.causal = d->causal;
+    p.block = resolve_block(d);
+    return p;
+}
+
+int64_t nnz_bound(const MaskParams& p) {
+    int64_t total = 0;
+    for (int64_t q = 0; q < p.N; ++q) {
+        if (p.mode == RIS_STOCHASTIC) {
+            const int64_t n = p.causal ? q + 1 : p.N;
+            const int64_t k = ris::row_count(p.ppm, n) * p.n_seeds;
+            total += k < n ? k : n;
+        } else {
+            const int64_t start = (q / p.block) * (int64_t)p.block;
+            const int64_t clique = q - start + 1;
+            int64_t kg = ris::row_count(p.ppm, q + 1) - clique;
+            if (kg < 0) kg = 0;
+            if (kg > start) kg = start;
+            const int64_t g = kg * p.n_seeds;
+            total += clique + (g < start ? g : start);
+        }
+    }
+    return total * p.heads;
+}
+
+int hip_status(hipError_t e) { return e == hipSuccess ? RIS_OK : RIS_E_HIP; }
+
+}  // namespace
+
+extern "C" {
+
+int ris_version(void) { return (1 << 16) | 0; }
+
+const char* ris_status_string(int status) {
+    switch (status) {
+        case RIS_OK: return "RIS_OK";
+        case RIS_E_ARG: return "RIS_E_ARG: null pointer or out-of-range argument";
+        case RIS_E_SHAPE: return "RIS_E_SHAPE: inconsistent sizes";
+        case RIS_E_DTYPE: return "RIS_E_DTYPE: unknown element type";
+        case RIS_E_CAPACITY: return "RIS_E_CAPACITY: col_idx capacity below nnz";
+        case RIS_E_UNSUPPORTED: return "RIS_E_UNSUPPORTED: valid request outside what is implemented";
+        case RIS_E_HIP: return "RIS_E_HIP: HIP runtime error";
+        default: return "unknown ris_status";
+    }
+}
+
+int64_t ris_mask_nnz_bound(const ris_mask_desc* desc) {
+    const int st = validate_mask(desc);
+    if (st != RIS_OK) return st;
+    return nnz_bound(make_params(desc));
+}
+
+int ris_mask_build(const ris_mask_desc* desc, int64_t* row_ptr, int32_t* col_idx,
+                   int64_t col_capacity, void* stream) {
+    const int st = validate_mask(desc);
+    if (st != RIS_OK) return st;
+    if (!row_ptr) return RIS_E_ARG;
+    const MaskParams p = make_params(desc);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (!col_idx) return hip_status(ris::launch_mask_count(p, row_ptr, s));
+    if (col_capacity < 0) return RIS_E_ARG;
+    if (col_capacity < nnz_bound(p)) {
+        int64_t nnz = 0;
+        const int64_t rows = (int64_t)p.heads * p.N;
+        if (hipMemcpyAsync(&nnz, row_ptr + rows, sizeof(nnz), hipMemcpyDeviceToHost, s) != hipSuccess)
+            return RIS_E_HIP;
+        if (hipStreamSynchronize(s) != hipSuccess) return RIS_E_HIP;
+        if (nnz > col_capacity || nnz < 0) return RIS_E_CAPACITY;
+    }
+    return hip_status(ris::launch_mask_fill(p, row_ptr, col_idx, col_capacity, s));
+}
+
+int ris_rope(void* x, int32_t dtype, int32_t heads, int64_t N, int32_t D, int64_t pos0,
+             const ris_rope_desc* desc, void* stream) {
+    if (!x || !desc) return RIS_E_ARG;
+    if (dtype != RIS_F32 && dtype != RIS_BF16) return RIS_E_DTYPE;
+    if (heads < 1 || N < 1 || pos0 < 0) return RIS_E_ARG;
+    if (D < 2 || (D & 1) || D / 2 > ris::kMaxRopeHalf) return RIS_E_SHAPE;
+    if (desc->kind < RIS_ROPE_PLAIN || desc->kind > RIS_ROPE_YARN) return RIS_E_ARG;
+    if (!(desc->base > 1.0) || !isfinite(desc->base)) return RIS_E_ARG;
+    if (!(desc->factor >= 0.0) || !isfinite(desc->factor)) return RIS_E_ARG;
+    if (!(desc->beta_slow >= 0.0) || !(desc->beta_fast >= 0.0)) return RIS_E_ARG;
+    if (desc->kind != RIS_ROPE_PLAIN && desc->orig_max_pos < 1) return RIS_E_ARG;
+    if (N > (1ll << 32) || pos0 > (1ll << 52)) return RIS_E_ARG;
+
+    // Factor: requested window / native limit (at least 1) unless given.
+    double s = desc->factor;
+    if (desc->kind != RIS_ROPE_PLAIN && !(s > 0.0)) {
+        s = (double)(pos0 + N) / (double)desc->orig_max_pos;
+        if (s < 1.0) s = 1.0;
+    }
+    ris::RopeTable tab;
+    const int half = D / 2;
+    const double base = desc->base;
+    for (int i = 0; i < half; ++i) {
+        const double plain = 1.0 / pow(base, 2.0 * i / D);
+        double f = plain;
+        if (desc->kind == RIS_ROPE_LINEAR) {
+            f = plain / s;
+        } else if (desc->kind == RIS_ROPE_YARN) {
+            const double b_slow = desc->beta_slow > 0.0 ? desc->beta_slow : 1.0;
+            const double b_fast = desc->beta_fast > 0.0 ? desc->beta_fast : 32.0;
+            const double L0 = (double)desc->orig_max_pos;
+            const double c_fast = D * log(L0 / (b_fast * 2.0 * M_PI)) / (2.0 * log(base));
+            const double c_slow = D * log(L0 / (b_slow * 2.0 * M_PI)) / (2.0 * log(base));
+            double lo = floor(c_fast), hi = ceil(c_slow);
+            if (lo < 0.0) lo = 0.0;
+            if (hi > D - 1) hi = D - 1;
+            if (lo == hi) hi += 0.001;
+            double t = (i - lo) / (hi - lo);
+            t = t < 0.0 ? 0.0 : (t > 1.0 ? 1.0 : t);
+            f = t * (plain / s) + (1.0 - t) * plain;
+        }
+        tab.inv_freq[i] = f;
+    }
+    tab.mscale = (desc->kind == RIS_ROPE_YARN && s > 1.0) ? 0.1 * log(s) + 1.0 : 1.0;
+    return hip_status(ris::launch_rope(x, dtype == RIS_BF16, heads, N, D, pos0, tab,
+                                       static_cast<hipStream_t>(stream)));
+}
+
+int ris_sparse_attn(const void* Q, const void* K, const void* V, const int64_t* row_ptr,
+                    const int32_t* col_idx, void* out, const ris_attn_desc* desc, void* stream) {
+    if (!Q || !K || !V || !row_ptr || !col_idx || !out || !desc) return RIS_E_ARG;
+    const ris_attn_desc& d = *desc;
+    if ((d.dtype_in != RIS_F32 && d.dtype_in != RIS_BF16) ||
+        (d.dtype_out != RIS_F32 && d.dtype_out != RIS_BF16))
+        return RIS_E_DTYPE;
+    if (d.Hq < 1 || d.Hkv < 1 || d.N < 1 || d.N > RIS_MAX_N) return RIS_E_ARG;
+    if (d.Hq % d.Hkv != 0) return RIS_E_SHAPE;
+    if (d.Hq / d.Hkv > 8) return RIS_E_UNSUPPORTED;
+    if (d.D != 64 && d.D != 128) return RIS_E_UNSUPPORTED;
+    if (!(d.scale >= 0.0f) || !isfinite(d.scale)) return RIS_E_ARG;
+    if (d.mode != RIS_STOCHASTIC && d.mode != RIS_STRUCTURAL) return RIS_E_ARG;
+    if (d.algo < RIS_ATTN_AUTO || d.algo > RIS_ATTN_TILE) return RIS_E_ARG;
+    if ((int64_t)d.Hkv * d.N > 0x7FFFFFFFll) return RIS_E_UNSUPPORTED;
+
+    ris::AttnParams a;
+    a.Q = Q; a.K = K; a.V = V;
+    a.row_ptr = row_ptr; a.col_idx = col_idx; a.out = out;
+    a.N = d.N; a.Hq = d.Hq; a.Hkv = d.Hkv; a.G = d.Hq / d.Hkv; a.D = d.D;
+    a.in_bf16 = d.dtype_in == RIS_BF16; a.out_bf16 = d.dtype_out == RIS_BF16;
+    a.mode = d.mode; a.block = d.block; a.causal = d.causal;
+    a.scale = d.scale > 0.0f ? d.scale : 1.0f / sqrtf((float)d.D);
+    if (d.algo == RIS_ATTN_TILE) return RIS_E_UNSUPPORTED;
+    return hip_status(ris::launch_attn_gather(a, static_cast<hipStream_t>(stream)));
+}
+
+}  // extern "C"

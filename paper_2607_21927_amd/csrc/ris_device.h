@@ -1,0 +1,164 @@
+// Device helpers shared by the RIS kernels (gfx950, wave64).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace ris {
+
+// ---------------------------------------------------------------------------
+// Counter-based hashing of (seed, layer, kv_head, query) rows.
+// ---------------------------------------------------------------------------
+
+// Philox4x64-10 (Salmon et al., SC'11): two 64x64->128 multiplies per round,
+// Weyl-sequence key schedule between rounds.
+struct Philox4x64Out { uint64_t v[4]; };
+
+__device__ __forceinline__ Philox4x64Out philox4x64_10(uint64_t c0, uint64_t c1, uint64_t c2,
+                                                       uint64_t c3, uint64_t k0, uint64_t k1) {
+    constexpr uint64_t kMul0 = 0xD2E7470EE14C6C93ull, kMul1 = 0xCA5A826395121157ull;
+    constexpr uint64_t kWeyl0 = 0x9E3779B97F4A7C15ull, kWeyl1 = 0xBB67AE8584CAA73Bull;
+#pragma unroll
+    for (int r = 0; r < 10; ++r) {
+        if (r) { k0 += kWeyl0; k1 += kWeyl1; }
+        const uint64_t lo0 = kMul0 * c0, hi0 = __umul64hi(kMul0, c0);
+        const uint64_t lo1 = kMul1 * c2, hi1 = __umul64hi(kMul1, c2);
+        const uint64_t n0 = hi1 ^ c1 ^ k0, n2 = hi0 ^ c3 ^ k1;
+        c0 = n0; c1 = lo1; c2 = n2; c3 = lo0;
+    }
+    Philox4x64Out o; o.v[0] = c0; o.v[1] = c1; o.v[2] = c2; o.v[3] = c3;
+    return o;
+}
+
+// Six 32-bit round keys of one row: the first three Philox outputs, low word
+// first; key = (seed, 0), counter = (q, kv_head, layer, 0).
+__device__ __forceinline__ void row_round_keys(uint64_t seed, uint64_t q, uint64_t kv_head,
+                                               uint64_t layer, uint32_t rk[6]) {
+    const Philox4x64Out o = philox4x64_10(q, kv_head, layer, 0ull, seed, 0ull);
+#pragma unroll
+    for (int i = 0; i < 3; ++i) {
+        rk[2 * i] = (uint32_t)o.v[i];
+        rk[2 * i + 1] = (uint32_t)(o.v[i] >> 32);
+    }
+}
+
+// MurmurHash3 32-bit finaliser.
+__device__ __forceinline__ uint32_t fmix32(uint32_t h) {
+    h ^= h >> 16; h *= 0x85EBCA6Bu;
+    h ^= h >> 13; h *= 0xC2B2AE35u;
+    h ^= h >> 16;
+    return h;
+}
+
+// Keyed permutation of [0, n) used for exact-k draws: balanced six-round
+// Feistel network on m-bit words (m even, h = m/2) restricted to [0, n) by
+// cycle walking.
+struct FeistelDomain {
+    uint32_t n;      // pool size (>= 1)
+    uint32_t half;   // h
+    uint32_t mask;   // 2^h - 1
+    uint32_t size;   // 2^m
+};
+
+__host__ __device__ __forceinline__ FeistelDomain make_domain(uint32_t n) {
+    uint32_t bits = 0;
+    for (uint32_t v = n > 0 ? n - 1 : 0; v; v >>= 1) ++bits;
+    if (bits < 2) bits = 2;
+    bits += bits & 1u;
+    FeistelDomain d;
+    d.n = n; d.half = bits / 2; d.mask = (1u << d.half) - 1u; d.size = 1u << bits;
+    return d;
+}
+
+__device__ __forceinline__ uint32_t feistel6(uint32_t x, const uint32_t rk[6], uint32_t half,
+                                             uint32_t mask) {
+    uint32_t L = x >> half, R = x & mask;
+#pragma unroll
+    for (int r = 0; r < 6; ++r) {
+        const uint32_t f = fmix32(R ^ rk[r]) & mask;
+        const uint32_t t = L ^ f;
+        L = R; R = t;
+    }
+    return (L << half) | R;
+}
+
+// P(j) for j < n.  The walk is bounded by the domain size (a permutation's
+// cycle through j returns to j within that many steps), so it always ends.
+__device__ __forceinline__ uint32_t permute(uint32_t j, const uint32_t rk[6], const FeistelDomain& d) {
+    uint32_t x = feistel6(j, rk, d.half, d.mask);
+    for (uint32_t it = 1; x >= d.n && it < d.size; ++it) x = feistel6(x, rk, d.half, d.mask);
+    return x < d.n ? x : 0u;
+}
+
+// Count rule: clamp(round_half_up(ppm * n / 1e6), 1, n).
+__host__ __device__ __forceinline__ int64_t row_count(int64_t ppm, int64_t n) {
+    int64_t k = (ppm * n + 500000) / 1000000;
+    if (k < 1) k = 1;
+    if (k > n) k = n;
+    return k;
+}
+
+// ---------------------------------------------------------------------------
+// Numeric helpers.
+// ---------------------------------------------------------------------------
+
+__device__ __forceinline__ float bf16_to_f32(uint16_t b) {
+    return __uint_as_float(((uint32_t)b) << 16);
+}
+
+// Round to nearest even; NaN stays NaN.
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
+    const uint32_t u = __float_as_uint(f);
+    if ((u & 0x7F800000u) == 0x7F800000u && (u & 0x007FFFFFu)) return (uint16_t)((u >> 16) | 0x40u);
+    return (uint16_t)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
+}
+
+// ---------------------------------------------------------------------------
+// Wavefront (64-lane) reductions via DPP; every lane receives the result.
+// ---------------------------------------------------------------------------
+
+// Lanes whose row is disabled by ROW_MASK (or whose source is out of range)
+// receive `identity`, so op(v, result) leaves them unchanged.
+template <int CTRL, int ROW_MASK = 0xF>
+__device__ __forceinline__ float dpp(float v, float identity) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(identity), __float_as_int(v),
+                                                      CTRL, ROW_MASK, 0xF, false));
+}
+
+__device__ __forceinline__ float wave_max(float v) {
+    const float id = -INFINITY;
+    v = fmaxf(v, dpp<0xB1>(v, id));          // quad_perm [1,0,3,2]
+    v = fmaxf(v, dpp<0x4E>(v, id));          // quad_perm [2,3,0,1]
+    v = fmaxf(v, dpp<0x141>(v, id));         // row_half_mirror
+    v = fmaxf(v, dpp<0x140>(v, id));         // row_mirror: each lane holds its row of 16
+    v = fmaxf(v, dpp<0x142, 0xA>(v, id));    // row_bcast:15 into rows 1 and 3
+    v = fmaxf(v, dpp<0x143, 0xC>(v, id));    // row_bcast:31 into rows 2 and 3
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+    v += dpp<0xB1>(v, 0.0f);
+    v += dpp<0x4E>(v, 0.0f);
+    v += dpp<0x141>(v, 0.0f);
+    v += dpp<0x140>(v, 0.0f);
+    v += dpp<0x142, 0xA>(v, 0.0f);
+    v += dpp<0x143, 0xC>(v, 0.0f);
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
+}
+
+__device__ __forceinline__ uint32_t wave_sum_u32(uint32_t v) {
+    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
+    return v;
+}
+
+// Inclusive prefix sum across the 64 lanes of a wave.
+__device__ __forceinline__ uint32_t wave_inclusive_scan(uint32_t v, int lane) {
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const uint32_t t = __shfl_up(v, off);
+        if (lane >= off) v += t;
+    }
+    return v;
+}
+
+}  // namespace ris

@@ -1,0 +1,183 @@
+"""Python binding of libris.so (ctypes).
+
+Argument marshalling only: every step runs in the HIP library.  Tensors are
+torch tensors used as device memory; streams are torch's current HIP stream
+unless one is given.  A missing library raises -- there is no fallback.
+"""
+import ctypes
+import os
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libris.so")
+
+OK, E_ARG, E_SHAPE, E_DTYPE, E_CAPACITY, E_UNSUPPORTED, E_HIP = 0, -1, -2, -3, -4, -5, -6
+STOCHASTIC, STRUCTURAL = 0, 1
+F32, BF16 = 0, 1
+ROPE_PLAIN, ROPE_LINEAR, ROPE_YARN = 0, 1, 2
+ATTN_AUTO, ATTN_GATHER, ATTN_TILE = 0, 1, 2
+MAX_N = 262144
+
+
+class RisError(RuntimeError):
+    def __init__(self, status, what):
+        super().__init__(f"{what}: {status_string(status)} ({status})")
+        self.status = status
+
+
+class MaskDesc(ctypes.Structure):
+    _fields_ = [("mode", ctypes.c_int32), ("density_ppm", ctypes.c_int32),
+                ("seed", ctypes.c_uint64), ("n_seeds", ctypes.c_int32),
+                ("layer", ctypes.c_int32), ("N", ctypes.c_int64), ("heads", ctypes.c_int32),
+                ("causal", ctypes.c_int32), ("block", ctypes.c_int32)]
+
+
+class RopeDesc(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int32), ("base", ctypes.c_double),
+                ("orig_max_pos", ctypes.c_int64), ("factor", ctypes.c_double),
+                ("beta_slow", ctypes.c_double), ("beta_fast", ctypes.c_double)]
+
+
+class AttnDesc(ctypes.Structure):
+    _fields_ = [("dtype_in", ctypes.c_int32), ("dtype_out", ctypes.c_int32),
+                ("Hq", ctypes.c_int32), ("Hkv", ctypes.c_int32), ("N", ctypes.c_int64),
+                ("D", ctypes.c_int32), ("scale", ctypes.c_float), ("mode", ctypes.c_int32),
+                ("block", ctypes.c_int32), ("causal", ctypes.c_int32), ("algo", ctypes.c_int32)]
+
+
+_lib = None
+
+
+def lib():
+    """Load libris.so once; raise if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with __graft_entry__.build()")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+        L.ris_mask_build.argtypes = [ctypes.POINTER(MaskDesc), vp, vp, i64, vp]
+        L.ris_mask_build.restype = ctypes.c_int
+        L.ris_mask_nnz_bound.argtypes = [ctypes.POINTER(MaskDesc)]
+        L.ris_mask_nnz_bound.restype = i64
+        L.ris_rope.argtypes = [vp, i32, i32, i64, i32, i64, ctypes.POINTER(RopeDesc), vp]
+        L.ris_rope.restype = ctypes.c_int
+        L.ris_sparse_attn.argtypes = [vp, vp, vp, vp, vp, vp, ctypes.POINTER(AttnDesc), vp]
+        L.ris_sparse_attn.restype = ctypes.c_int
+        L.ris_status_string.argtypes = [ctypes.c_int]
+        L.ris_status_string.restype = ctypes.c_char_p
+        L.ris_version.argtypes = []
+        L.ris_version.restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+EXPORTS = ("ris_mask_build", "ris_mask_nnz_bound", "ris_rope", "ris_sparse_attn",
+           "ris_status_string", "ris_version")
+
+
+def status_string(status):
+    return lib().ris_status_string(int(status)).decode()
+
+
+def version():
+    return lib().ris_version()
+
+
+def _check(status, what):
+    if status != OK:
+        raise RisError(status, what)
+
+
+def _stream(stream):
+    if stream is not None:
+        return ctypes.c_void_p(stream if isinstance(stream, int) else stream.cuda_stream)
+    import torch
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None else ctypes.c_void_p(0)
+
+
+def _dtype_code(t):
+    import torch
+    if t.dtype == torch.float32:
+        return F32
+    if t.dtype == torch.bfloat16:
+        return BF16
+    raise TypeError(f"unsupported dtype {t.dtype} (float32 or bfloat16)")
+
+
+def _need_device(*ts):
+    for t in ts:
+        if t is not None and (not t.is_cuda or not t.is_contiguous()):
+            raise ValueError("tensors must be contiguous GPU tensors")
+
+
+def mask_desc(mode, density_ppm, N, heads, n_seeds=1, seed=0, layer=0, causal=1, block=0):
+    return MaskDesc(mode, density_ppm, seed, n_seeds, layer, N, heads, causal, block)
+
+
+def mask_nnz_bound(desc):
+    v = lib().ris_mask_nnz_bound(ctypes.byref(desc))
+    if v < 0:
+        raise RisError(int(v), "ris_mask_nnz_bound")
+    return int(v)
+
+
+def mask_build(desc, row_ptr, col_idx=None, col_capacity=None, stream=None):
+    """ris_mask_build: count phase when col_idx is None, else fill phase."""
+    import torch
+    _need_device(row_ptr, col_idx)
+    if row_ptr.dtype != torch.int64 or row_ptr.numel() != desc.heads * desc.N + 1:
+        raise ValueError("row_ptr must be int64[heads*N + 1]")
+    if col_idx is not None and col_idx.dtype != torch.int32:
+        raise ValueError("col_idx must be int32")
+    cap = col_idx.numel() if (col_idx is not None and col_capacity is None) else (col_capacity or 0)
+    _check(lib().ris_mask_build(ctypes.byref(desc), _ptr(row_ptr), _ptr(col_idx), cap,
+                                _stream(stream)), "ris_mask_build")
+
+
+def rope(x, desc, pos0=0, stream=None):
+    """ris_rope on x [heads, N, D] in place."""
+    _need_device(x)
+    H, N, D = x.shape
+    _check(lib().ris_rope(_ptr(x), _dtype_code(x), H, N, D, pos0, ctypes.byref(desc),
+                          _stream(stream)), "ris_rope")
+    return x
+
+
+def rope_desc(kind, base, orig_max_pos=0, factor=0.0, beta_slow=0.0, beta_fast=0.0):
+    return RopeDesc(kind, base, orig_max_pos, factor, beta_slow, beta_fast)
+
+
+def attn_desc(Q, K, out, mode=STOCHASTIC, block=0, causal=1, scale=0.0, algo=ATTN_AUTO):
+    Hq, N, D = Q.shape
+    return AttnDesc(_dtype_code(Q), _dtype_code(out), Hq, K.shape[0], N, D, scale, mode,
+                    block, causal, algo)
+
+
+def sparse_attn(Q, K, V, row_ptr, col_idx, out, desc, stream=None):
+    """ris_sparse_attn: out[Hq, N, D] from the CSR sets."""
+    _need_device(Q, K, V, row_ptr, col_idx, out)
+    if not (Q.dtype == K.dtype == V.dtype):
+        raise TypeError("Q, K, V must share a dtype")
+    _check(lib().ris_sparse_attn(_ptr(Q), _ptr(K), _ptr(V), _ptr(row_ptr), _ptr(col_idx),
+                                 _ptr(out), ctypes.byref(desc), _stream(stream)),
+           "ris_sparse_attn")
+    return out
+
+
+def build_csr(desc, device="cuda", stream=None, use_bound=False):
+    """Both phases of ris_mask_build; returns (row_ptr, col_idx) on the device.
+
+    use_bound sizes col_idx from the host-side bound (no read-back between
+    the phases); otherwise the exact nnz is read back (one 8-byte copy).
+    """
+    import torch
+    row_ptr = torch.empty(desc.heads * desc.N + 1, dtype=torch.int64, device=device)
+    mask_build(desc, row_ptr, None, stream=stream)
+    cap = mask_nnz_bound(desc) if use_bound else int(row_ptr[-1].item())
+    col_idx = torch.empty(max(cap, 1), dtype=torch.int32, device=device)
+    mask_build(desc, row_ptr, col_idx, col_capacity=cap, stream=stream)
+    return row_ptr, col_idx

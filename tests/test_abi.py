@@ -1,0 +1,139 @@
+"""The C ABI library loads, exports every symbol its header declares, and
+validates arguments on the host (no GPU needed: every call here fails
+validation, or is host-only, before anything is launched)."""
+import ctypes
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+from oracle import geometry as o_geo
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "ris.h")
+
+
+@pytest.fixture(scope="module")
+def ris():
+    from paper_2607_21927_amd import _build, ris as r
+    if not os.path.exists(r.LIB_PATH):
+        _build.build()
+    r.lib()
+    return r
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(ris_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    assert names == sorted(["ris_mask_build", "ris_mask_nnz_bound", "ris_rope",
+                            "ris_sparse_attn", "ris_status_string", "ris_version"])
+
+
+def test_library_exports_every_declared_symbol(ris):
+    out = subprocess.run(["nm", "-D", "--defined-only", ris.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = set(re.findall(r"\sT\s(ris_\w+)", out))
+    for name in declared_functions():
+        assert name in exported, name
+        assert hasattr(ris.lib(), name)
+    assert set(ris.EXPORTS) == set(declared_functions())
+
+
+def test_status_strings_and_version(ris):
+    for code in (0, -1, -2, -3, -4, -5, -6):
+        assert ris.status_string(code).startswith("RIS_")
+    assert ris.status_string(123) == "unknown ris_status"
+    assert ris.version() >> 16 == 1
+
+
+def _mask(ris, **kw):
+    d = dict(mode=0, density_ppm=10_000, N=512, heads=1, n_seeds=1, seed=0, layer=0,
+             causal=1, block=0)
+    d.update(kw)
+    return ris.mask_desc(**d)
+
+
+@pytest.mark.parametrize("bad,code", [
+    (dict(density_ppm=0), -1), (dict(density_ppm=1_000_001), -1), (dict(n_seeds=0), -1),
+    (dict(n_seeds=4097), -1), (dict(N=0), -1), (dict(N=262145), -1), (dict(heads=0), -1),
+    (dict(layer=-1), -1), (dict(mode=2), -1), (dict(causal=2), -1), (dict(block=-1), -1),
+    (dict(mode=1, causal=0), -5),
+])
+def test_mask_validation(ris, bad, code):
+    d = _mask(ris, **bad)
+    L = ris.lib()
+    assert L.ris_mask_nnz_bound(ctypes.byref(d)) == code
+    fake = ctypes.c_void_p(0x1000)          # never dereferenced: validation fails first
+    assert L.ris_mask_build(ctypes.byref(d), fake, None, 0, None) == code
+
+
+def test_mask_null_pointers(ris):
+    L = ris.lib()
+    assert L.ris_mask_build(None, ctypes.c_void_p(0x1000), None, 0, None) == -1
+    d = _mask(ris)
+    assert L.ris_mask_build(ctypes.byref(d), None, None, 0, None) == -1
+    assert L.ris_mask_build(ctypes.byref(d), ctypes.c_void_p(0x1000), ctypes.c_void_p(0x2000),
+                            -5, None) == -1
+
+
+@pytest.mark.parametrize("mode,ppm,S,N,heads,block,causal", [
+    (0, 100_000, 1, 512, 1, 0, 1), (0, 10_000, 10, 4096, 2, 0, 1), (0, 10_000, 70, 3000, 2, 0, 1),
+    (1, 10_000, 10, 4096, 2, 64, 1), (1, 50_000, 10, 2000, 4, 64, 1), (1, 10_000, 3, 5000, 1, 0, 1),
+    (0, 250_000, 4, 777, 3, 0, 0), (1, 10**6, 2, 300, 1, 7, 1),
+])
+def test_nnz_bound_matches_oracle(ris, mode, ppm, S, N, heads, block, causal):
+    d = _mask(ris, mode=mode, density_ppm=ppm, n_seeds=S, N=N, heads=heads, block=block,
+              causal=causal)
+    spec = o_geo.MaskSpec(mode=mode, density_ppm=ppm, seed=0, n_seeds=S, layer=0, N=N,
+                          heads=heads, causal=causal, block=block)
+    assert ris.mask_nnz_bound(d) == o_geo.nnz_upper_bound(spec)
+
+
+def test_rope_validation(ris):
+    L = ris.lib()
+    x = ctypes.c_void_p(0x1000)
+    good = ris.rope_desc(ris.ROPE_YARN, 1e6, orig_max_pos=32768)
+    assert L.ris_rope(None, 0, 1, 8, 64, 0, ctypes.byref(good), None) == -1
+    assert L.ris_rope(x, 0, 1, 8, 64, 0, None, None) == -1
+    assert L.ris_rope(x, 7, 1, 8, 64, 0, ctypes.byref(good), None) == -3
+    assert L.ris_rope(x, 0, 1, 8, 63, 0, ctypes.byref(good), None) == -2
+    assert L.ris_rope(x, 0, 1, 8, 1024, 0, ctypes.byref(good), None) == -2
+    assert L.ris_rope(x, 0, 0, 8, 64, 0, ctypes.byref(good), None) == -1
+    assert L.ris_rope(x, 0, 1, 8, 64, -1, ctypes.byref(good), None) == -1
+    for bad in (ris.rope_desc(3, 1e6), ris.rope_desc(0, 1.0), ris.rope_desc(0, float("nan")),
+                ris.rope_desc(ris.ROPE_YARN, 1e6, orig_max_pos=0),
+                ris.rope_desc(ris.ROPE_LINEAR, 1e6, orig_max_pos=10, factor=-1.0)):
+        assert L.ris_rope(x, 0, 1, 8, 64, 0, ctypes.byref(bad), None) == -1
+
+
+def test_attn_validation(ris):
+    L = ris.lib()
+    p = ctypes.c_void_p(0x1000)
+
+    def call(**kw):
+        d = dict(dtype_in=1, dtype_out=0, Hq=12, Hkv=2, N=1024, D=128, scale=0.0, mode=0,
+                 block=0, causal=1, algo=0)
+        d.update(kw)
+        desc = ris.AttnDesc(*[d[f] for f, _ in ris.AttnDesc._fields_])
+        return L.ris_sparse_attn(p, p, p, p, p, p, ctypes.byref(desc), None)
+
+    assert call(Hq=12, Hkv=5) == -2
+    assert call(Hq=18, Hkv=2) == -5          # G = 9 > 8
+    assert call(D=96) == -5
+    assert call(dtype_in=4) == -3
+    assert call(dtype_out=-1) == -3
+    assert call(N=0) == -1
+    assert call(scale=-1.0) == -1
+    assert call(scale=float("inf")) == -1
+    assert call(algo=3) == -1
+    assert call(mode=5) == -1
+    d = ris.AttnDesc(1, 0, 12, 2, 64, 128, 0.0, 0, 0, 1, 0)
+    assert L.ris_sparse_attn(None, p, p, p, p, p, ctypes.byref(d), None) == -1
+    assert L.ris_sparse_attn(p, p, p, p, p, None, ctypes.byref(d), None) == -1

@@ -1,0 +1,98 @@
+"""GPU geometry (ris_mask_build) vs the oracle: bit-exact index sets."""
+import numpy as np
+import pytest
+
+from gpu_common import desc_of, gpu_csr, need_gpu, rows_of, say, spec_of, torch
+from oracle import geometry as o_geo
+
+pytestmark = pytest.mark.gpu
+
+SMALL = [
+    # mode, ppm, N, heads, S, seed, layer, causal, block
+    (0, 100_000, 512, 1, 1, 0, 0, 1, 0),           # the tiny workload
+    (0, 10_000, 4097, 2, 10, 0, 0, 1, 0),          # ragged N, 10 seeds
+    (1, 10_000, 4097, 2, 10, 0, 0, 1, 64),         # Structural, B = 64
+    (0, 10_000, 2048, 2, 70, 0, 0, 1, 0),          # 70-seed ensemble
+    (1, 50_000, 3000, 4, 10, 0, 5, 1, 64),         # TinyLlama-like, layer 5
+    (1, 10_000, 5000, 1, 3, 0, 0, 1, 0),           # paper block rule
+    (0, 250_000, 777, 3, 4, 2**63 + 5, 0, 0, 0),   # non-causal, large seed
+    (0, 10**6, 300, 2, 3, 0, 0, 1, 0),             # 100%: causal triangle
+    (1, 10**6, 300, 1, 2, 0, 0, 1, 7),
+    (1, 30_000, 400, 1, 5, 0, 0, 1, 1),            # B = 1: clique is q alone
+    (1, 30_000, 400, 1, 5, 0, 0, 1, 1000),         # B > N: one block
+    (0, 1, 1000, 1, 300, 9, 2, 1, 0),              # k = 1 rows, 300 seeds (batches of 64)
+    (0, 500_000, 1, 1, 4, 0, 0, 1, 0),             # N = 1
+    (0, 500_000, 2, 1, 4, 0, 0, 1, 0),             # N = 2
+]
+
+
+@pytest.mark.parametrize("cfg", SMALL)
+def test_mask_bit_exact_small(cfg):
+    ris = need_gpu()
+    mode, ppm, N, heads, S, seed, layer, causal, block = cfg
+    sp = spec_of(mode, ppm, N, heads, S, seed, layer, causal, block)
+    say(f"mask parity {cfg}")
+    rp, ci = gpu_csr(ris, sp)
+    want_rp, want_ci = o_geo.build_csr(sp)
+    rp = rp.cpu().numpy()
+    assert np.array_equal(rp, want_rp)
+    assert np.array_equal(ci.cpu().numpy()[: rp[-1]], want_ci)
+
+
+def test_mask_bound_sized_fill_and_determinism():
+    ris = need_gpu()
+    sp = spec_of(0, 10_000, 3000, 2, 10)
+    rp1, ci1 = gpu_csr(ris, sp, use_bound=True)
+    rp2, ci2 = gpu_csr(ris, sp, use_bound=False)
+    nnz = int(rp1[-1].item())
+    assert torch.equal(rp1, rp2)
+    assert torch.equal(ci1[:nnz], ci2[:nnz])
+    rp3, ci3 = gpu_csr(ris, sp)
+    assert torch.equal(rp2, rp3) and torch.equal(ci2, ci3)
+
+
+def test_mask_capacity_error_writes_nothing():
+    ris = need_gpu()
+    sp = spec_of(0, 50_000, 2000, 2, 5)
+    d = desc_of(ris, sp)
+    rp = torch.empty(sp.heads * sp.N + 1, dtype=torch.int64, device="cuda")
+    ris.mask_build(d, rp)
+    nnz = int(rp[-1].item())
+    small = torch.full((nnz - 1,), -7, dtype=torch.int32, device="cuda")
+    with pytest.raises(ris.RisError) as e:
+        ris.mask_build(d, rp, small)
+    assert e.value.status == ris.E_CAPACITY
+    torch.cuda.synchronize()
+    assert bool((small == -7).all())
+    exact = torch.empty(nnz, dtype=torch.int32, device="cuda")
+    ris.mask_build(d, rp, exact)
+    assert np.array_equal(exact.cpu().numpy(), o_geo.build_csr(sp)[1])
+
+
+@pytest.mark.parametrize("name", ["qwen2_32k_stochastic", "qwen2_32k_structural",
+                                  "qwen2_64k_stochastic_yarn", "tinyllama_64k_structural"])
+def test_mask_full_size(name):
+    """Full-size geometry of each workload: every row's size within its
+    closed-form bounds, nnz consistent, sampled rows bit-exact."""
+    from synth import WORKLOADS
+    from gpu_common import sample_rows
+    ris = need_gpu()
+    w = WORKLOADS[name]
+    layer = 21 if w.layers > 1 else 0
+    sp = spec_of(w.mode, w.density_ppm, w.N, w.Hkv, w.n_seeds, w.seed, layer, 1, w.block)
+    say(f"full-size mask {name} layer {layer}")
+    rp_d, ci_d = gpu_csr(ris, sp, use_bound=True)
+    rp = rp_d.cpu().numpy()
+    counts = np.diff(rp)
+    q = np.tile(np.arange(w.N), w.Hkv)
+    n, kk, start = o_geo._pool_and_draws(sp, q)
+    lo, hi = kk.copy(), np.minimum(n, w.n_seeds * kk)
+    if w.mode == o_geo.STRUCTURAL:
+        lo, hi = lo + (q - start + 1), hi + (q - start + 1)
+    assert rp[0] == 0 and np.all(counts >= lo) and np.all(counts <= hi)
+    rows = sample_rows(w.N, w.Hkv, k_each=10)
+    got = rows_of(rp, ci_d, [h * w.N + qq for h, qq in rows])
+    for (h, qq), g in zip(rows, got):
+        want = o_geo.row_sets(sp, h, np.array([qq]))[0]
+        assert np.array_equal(g, want), (h, qq)
+    say(f"  nnz = {rp[-1]} ({rp[-1] / (w.Hkv * w.N * (w.N + 1) / 2):.4f} of causal pairs)")

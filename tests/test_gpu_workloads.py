@@ -1,0 +1,71 @@
+"""End-to-end hot path at the workloads' full sizes (RoPE -> geometry ->
+sparse attention, bf16 in / bf16 out, the launch configuration the benchmark
+times), checked on sampled rows the oracle computes one by one."""
+import numpy as np
+import pytest
+
+from gpu_common import desc_of, need_gpu, sample_rows, say, spec_of, torch
+from oracle import attention as o_att
+from oracle import geometry as o_geo
+from oracle import rope as o_rope
+from synth import ROPE_NONE, WORKLOADS, gaussian_qkv, needle_plan, plant_needles, to_bf16
+
+pytestmark = pytest.mark.gpu
+
+
+def gpu_pipeline(ris, w, Qb, Kb, Vb, layer):
+    qd, kd, vd = Qb.cuda(), Kb.cuda(), Vb.cuda()
+    if w.rope != ROPE_NONE:
+        rd = ris.rope_desc(w.rope, w.rope_base, orig_max_pos=w.rope_orig, factor=w.rope_factor)
+        ris.rope(qd, rd)
+        ris.rope(kd, rd)
+    if w.needles:
+        Qn = plant_needles(qd.float().cpu().numpy(), kd.float().cpu().numpy(), needle_plan(w.N))
+        qd = to_bf16(Qn.astype(np.float32)).cuda()
+    sp = spec_of(w.mode, w.density_ppm, w.N, w.Hkv, w.n_seeds, w.seed, layer, 1, w.block)
+    rp, ci = ris.build_csr(desc_of(ris, sp), "cuda", use_bound=True)
+    out = torch.empty(w.Hq, w.N, w.D, dtype=torch.bfloat16, device="cuda")
+    ris.sparse_attn(qd, kd, vd, rp, ci, out,
+                    ris.attn_desc(qd, kd, out, mode=w.mode, block=w.block))
+    torch.cuda.synchronize()
+    return sp, out
+
+
+@pytest.mark.parametrize("name", ["qwen2_32k_stochastic", "qwen2_32k_structural",
+                                  "qwen2_64k_stochastic_yarn", "tinyllama_64k_structural"])
+def test_workload_end_to_end(name):
+    ris = need_gpu()
+    w = WORKLOADS[name]
+    layer = 21 if w.layers > 1 else 0
+    say(f"workload {name}: Hq={w.Hq} Hkv={w.Hkv} N={w.N} D={w.D} layer={layer}")
+    Q, K, V = gaussian_qkv(w.Hq, w.Hkv, w.N, w.D, seed=0)
+    Qb, Kb, Vb = to_bf16(Q), to_bf16(K), to_bf16(V)
+    del Q, K, V
+    sp, out = gpu_pipeline(ris, w, Qb, Kb, Vb, layer)
+
+    rows = sample_rows(w.N, w.Hq, k_each=6, seed=1)
+    qs = np.array(sorted({q for _, q in rows}))
+    Kr = Kb.float().numpy()
+    Vr = Vb.float().numpy()
+    if w.rope != ROPE_NONE:
+        s = o_rope.scale_factor(w.rope_factor, w.N, w.rope_orig) if w.rope != o_rope.PLAIN else 1.0
+        rot = dict(kind=w.rope, base=w.rope_base, s=s, orig_max_pos=w.rope_orig)
+        Kr = to_bf16(o_rope.apply(Kr, **rot).astype(np.float32)).float().numpy()
+        if w.needles:
+            Qr = to_bf16(o_rope.apply(Qb.float().numpy(), **rot).astype(np.float32)).float().numpy()
+            Qr = to_bf16(plant_needles(Qr, Kr, needle_plan(w.N)).astype(np.float32)).float().numpy()
+        else:
+            Qr = np.zeros((w.Hq, w.N, w.D), dtype=np.float32)
+            Qr[:, qs] = to_bf16(o_rope.apply(Qb.float().numpy()[:, qs], positions=qs, **rot)
+                                .astype(np.float32)).float().numpy()
+    else:
+        Qr = Qb.float().numpy()
+    G = w.Hq // w.Hkv
+    got = out.float().cpu().numpy()
+    worst = 0.0
+    for h, q in rows:
+        I = o_geo.row_sets(sp, h // G, np.array([q]))[0]
+        want = o_att.attend_one(Qr[h, q], Kr[h // G, I], Vr[h // G, I], 1 / np.sqrt(w.D))
+        worst = max(worst, float(np.abs(got[h, q] - want).max()))
+    say(f"  {len(rows)} sampled rows, max err {worst:.3e}")
+    assert worst <= 2e-2
