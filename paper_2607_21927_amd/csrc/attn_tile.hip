@@ -1,0 +1,311 @@
+// Sparse attention, tiled form: one workgroup per (kv_head g, 32 consecutive
+// query rows), one wavefront per query head of the GQA group.
+//
+// When a row's unified set covers a sizeable share of its keys (a 70-seed
+// ensemble at 1% reaches ~50%), the sets of 32 neighbouring rows together
+// touch nearly every key block, so the work is a dense contraction under a
+// mask.  For every 64-key block the workgroup
+//   1. stages K[g, block] in LDS (row-major) and V[g, block] transposed, once
+//      for all 32 rows x G heads;
+//   2. turns each row's CSR entries that fall in the block into per-key tags
+//      in LDS (a window of 64 entries from the row's cursor suffices, the
+//      rows being ascending and unique);
+//   3. per wave (head h): S^T = K_blk Q_h^T on MFMA (32x32x16 bf16), masked by
+//      the tags, one online-softmax update per query over the block, and
+//      O^T += V_blk^T P^T on MFMA with P kept in registers.
+// Each lane owns one query column of S^T and of O^T, so the running max and
+// sum are per lane (plus one exchange with the lane 32 away): every index of a
+// row's set enters one normalisation (Pre-Fusion Unified Softmax; Methods,
+// "Hybrid Anchor and Pre-Fusion Unified Softmax").  In Structural mode the
+// block clique is the diagonal 64-key block: the dense local tile runs on
+// MFMA in the same softmax state as the sampled global keys.
+#include "ris_device.h"
+#include "ris_internal.h"
+
+namespace ris {
+namespace {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+
+constexpr int kRows = 32;   // query rows per tile (MFMA N)
+constexpr int kKeys = 64;   // keys per block
+
+__device__ __forceinline__ bf16x8_t as_bf16x8(uint4 v) {
+    return __builtin_bit_cast(bf16x8_t, v);
+}
+
+// v if keep, else zeros (the load itself always reads a valid address).
+__device__ __forceinline__ uint4 select4(bool keep, uint4 v) {
+    return keep ? v : make_uint4(0u, 0u, 0u, 0u);
+}
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+    return (uint32_t)f32_to_bf16(lo) | ((uint32_t)f32_to_bf16(hi) << 16);
+}
+
+template <int D, int G>
+__global__ __launch_bounds__(64 * G) void k_attn_tile(AttnParams a, float c) {
+    constexpr int NT = 64 * G;
+    constexpr int KS = D + 8;          // K row stride in LDS (bf16 elements)
+    constexpr int VS = kKeys + 4;      // V^T row stride
+    constexpr int TS = kKeys + 4;      // tag row stride
+    constexpr int RPW = (kRows + G - 1) / G;
+    constexpr int KSTEPS = D / 16;
+    constexpr int DT = D / 32;
+    __shared__ __align__(16) uint16_t Ks[kKeys * KS];
+    __shared__ __align__(16) uint16_t Vt[D * VS];
+    __shared__ __align__(16) uint16_t tags[kRows * TS];
+    __shared__ int64_t rstart[kRows];
+    __shared__ int32_t rlen[kRows];
+    __shared__ int32_t rcur[kRows];
+    __shared__ int32_t wcount[G];
+    __shared__ int32_t kb_range[2];
+
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int hf = lane >> 5, n = lane & 31;
+    const int64_t N = a.N;
+    const int64_t tiles = (N + kRows - 1) / kRows;
+    const int64_t bid = blockIdx.x;
+    const int64_t tile = tiles - 1 - bid / a.Hkv;     // late (heavy) tiles first
+    const int g = (int)(bid % a.Hkv);
+    const int64_t q0 = tile * kRows;
+    const int h = g * G + w;
+    const uint16_t* Kg = static_cast<const uint16_t*>(a.K) + (int64_t)g * N * D;
+    const uint16_t* Vg = static_cast<const uint16_t*>(a.V) + (int64_t)g * N * D;
+
+    // ---- per-row CSR extents, tags cleared
+    for (int i = tid; i < kRows * TS; i += NT) tags[i] = 0;
+    if (tid < kRows) {
+        const int64_t q = q0 + tid;
+        int64_t s = 0, L = 0;
+        if (q < N) {
+            s = a.row_ptr[g * N + q];
+            L = a.row_ptr[g * N + q + 1] - s;
+        }
+        rstart[tid] = s;
+        rlen[tid] = (int)L;
+        rcur[tid] = 0;
+    }
+    __syncthreads();
+    // Key-block range touched by any row: first and last entries of each row.
+    if (w == 0) {
+        int lo = 0x7FFFFFFF, hi = -1;
+        if (lane < kRows && rlen[lane] > 0) {
+            const int64_t nb = (N - 1) / kKeys;
+            int64_t f = a.col_idx[rstart[lane]] / kKeys;
+            int64_t l = a.col_idx[rstart[lane] + rlen[lane] - 1] / kKeys;
+            f = f < 0 ? 0 : (f > nb ? nb : f);
+            l = l < 0 ? 0 : (l > nb ? nb : l);
+            lo = (int)f;
+            hi = (int)l;
+        }
+        for (int off = 32; off > 0; off >>= 1) {
+            lo = min(lo, __shfl_xor(lo, off));
+            hi = max(hi, __shfl_xor(hi, off));
+        }
+        if (lane == 0) { kb_range[0] = lo; kb_range[1] = hi; }
+    }
+
+    // ---- this lane's query row of Q_h, as the B operand (k = dims)
+    bf16x8_t qf[KSTEPS];
+    {
+        const int64_t q = q0 + n;
+        const uint16_t* Qrow = static_cast<const uint16_t*>(a.Q) + ((int64_t)h * N + (q < N ? q : 0)) * D;
+#pragma unroll
+        for (int ks = 0; ks < KSTEPS; ++ks)
+            qf[ks] = as_bf16x8(select4(q < N, *reinterpret_cast<const uint4*>(Qrow + ks * 16 + 8 * hf)));
+    }
+    float m_run = -INFINITY, l_run = 0.f;
+    f32x16_t o[DT];
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) o[dt][r] = 0.f;
+    __syncthreads();
+
+    const int kb_lo = kb_range[0], kb_hi = kb_range[1];
+    for (int kb = kb_lo; kb <= kb_hi; ++kb) {
+        const int64_t k0 = (int64_t)kb * kKeys;
+        // ---- stage K (row-major) and V (transposed) for this block
+        for (int e = tid; e < kKeys * (D / 8); e += NT) {
+            const int key = e / (D / 8), ch = e % (D / 8);
+            const int64_t j = k0 + key;
+            const uint4 v = select4(j < N, *reinterpret_cast<const uint4*>(Kg + min(j, N - 1) * D + ch * 8));
+            *reinterpret_cast<uint4*>(&Ks[key * KS + ch * 8]) = v;
+        }
+        for (int e = tid; e < (kKeys / 2) * (D / 8); e += NT) {
+            const int p = e % (kKeys / 2), ch = e / (kKeys / 2);
+            const int64_t j0 = k0 + 2 * p;
+            const uint4 v0 = select4(j0 < N, *reinterpret_cast<const uint4*>(Vg + min(j0, N - 1) * D + ch * 8));
+            const uint4 v1 =
+                select4(j0 + 1 < N, *reinterpret_cast<const uint4*>(Vg + min(j0 + 1, N - 1) * D + ch * 8));
+            const uint32_t a0[4] = {v0.x, v0.y, v0.z, v0.w};
+            const uint32_t a1[4] = {v1.x, v1.y, v1.z, v1.w};
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                *reinterpret_cast<uint32_t*>(&Vt[(ch * 8 + 2 * k) * VS + 2 * p]) =
+                    (a0[k] & 0xFFFFu) | (a1[k] << 16);
+                *reinterpret_cast<uint32_t*>(&Vt[(ch * 8 + 2 * k + 1) * VS + 2 * p]) =
+                    (a0[k] >> 16) | (a1[k] & 0xFFFF0000u);
+            }
+        }
+        // ---- tags: keys of this block present in each row's set
+        const uint16_t tag = (uint16_t)(kb + 1);
+        int my_cnt = 0;
+#pragma unroll
+        for (int i = 0; i < RPW; ++i) {
+            const int r = w + G * i;
+            if (r < kRows) {
+                const int cur = rcur[r], len = rlen[r];
+                int64_t col = -1;
+                if (lane < len - cur) col = a.col_idx[rstart[r] + cur + lane];
+                const bool inb = col >= k0 && col < k0 + kKeys && col < N;
+                const uint64_t bal = __ballot(inb);
+                if (inb) tags[r * TS + (int)(col - k0)] = tag;
+                const int cnt = __popcll(bal);
+                if (lane == 0) rcur[r] = cur + cnt;
+                my_cnt += cnt;
+            }
+        }
+        if (lane == 0) wcount[w] = my_cnt;
+        __syncthreads();
+        int any = 0;
+#pragma unroll
+        for (int i = 0; i < G; ++i) any += wcount[i];
+
+        if (any) {
+            // ---- S^T[key, query] = K_blk Q_h^T
+            f32x16_t st[2];
+#pragma unroll
+            for (int t = 0; t < 2; ++t) {
+#pragma unroll
+                for (int r = 0; r < 16; ++r) st[t][r] = 0.f;
+#pragma unroll
+                for (int ks = 0; ks < KSTEPS; ++ks) {
+                    const bf16x8_t av =
+                        as_bf16x8(*reinterpret_cast<const uint4*>(&Ks[(32 * t + n) * KS + ks * 16 + 8 * hf]));
+                    st[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, qf[ks], st[t], 0, 0, 0);
+                }
+            }
+            // ---- mask, one online-softmax step for this lane's query
+            // st[t][4i + j] holds key 32t + 8i + 4hf + j of query n.
+            float mx = -INFINITY;
+#pragma unroll
+            for (int t = 0; t < 2; ++t) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const uint2 tg = *reinterpret_cast<const uint2*>(&tags[n * TS + 32 * t + 8 * i + 4 * hf]);
+                    const uint32_t tv[4] = {tg.x & 0xFFFFu, tg.x >> 16, tg.y & 0xFFFFu, tg.y >> 16};
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        const float s = tv[j] == tag ? st[t][4 * i + j] : -INFINITY;
+                        st[t][4 * i + j] = s;
+                        mx = fmaxf(mx, s);
+                    }
+                }
+            }
+            mx = fmaxf(mx, __shfl_xor(mx, 32));
+            const float m_new = fmaxf(m_run, mx);
+            const float m_use = m_new == -INFINITY ? 0.f : m_new;
+            const float mc = m_use * c;
+            const float corr = __builtin_amdgcn_exp2f(fmaf(m_run, c, -mc));
+            float rs = 0.f;
+#pragma unroll
+            for (int t = 0; t < 2; ++t)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const float p = __builtin_amdgcn_exp2f(fmaf(st[t][r], c, -mc));
+                    st[t][r] = p;
+                    rs += p;
+                }
+            rs += __shfl_xor(rs, 32);
+            l_run = l_run * corr + rs;
+            m_run = m_new;
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) o[dt][r] *= corr;
+            // ---- P^T as the B operand: k-step (t, u) holds keys
+            // 32t+16u+4hf+{0..3} and 32t+16u+8+4hf+{0..3}
+            bf16x8_t pb[2][2];
+#pragma unroll
+            for (int t = 0; t < 2; ++t)
+#pragma unroll
+                for (int u = 0; u < 2; ++u) {
+                    uint4 pk;
+                    pk.x = pack_bf16x2(st[t][8 * u + 0], st[t][8 * u + 1]);
+                    pk.y = pack_bf16x2(st[t][8 * u + 2], st[t][8 * u + 3]);
+                    pk.z = pack_bf16x2(st[t][8 * u + 4], st[t][8 * u + 5]);
+                    pk.w = pack_bf16x2(st[t][8 * u + 6], st[t][8 * u + 7]);
+                    pb[t][u] = as_bf16x8(pk);
+                }
+            // ---- O^T[d, query] += V_blk^T P^T
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+                for (int t = 0; t < 2; ++t)
+#pragma unroll
+                    for (int u = 0; u < 2; ++u) {
+                        const uint16_t* vrow = &Vt[(32 * dt + n) * VS + 32 * t + 16 * u + 4 * hf];
+                        const uint2 lo = *reinterpret_cast<const uint2*>(vrow);
+                        const uint2 hi = *reinterpret_cast<const uint2*>(vrow + 8);
+                        const bf16x8_t av = as_bf16x8(make_uint4(lo.x, lo.y, hi.x, hi.y));
+                        o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pb[t][u], o[dt], 0, 0, 0);
+                    }
+        }
+        __syncthreads();
+    }
+
+    // ---- normalise and store: o[dt][r] is dim 32dt + 8(r/4) + 4hf + r%4 of query n
+    const int64_t q = q0 + n;
+    if (q < N) {
+        const float inv = l_run > 0.f ? 1.0f / l_run : 0.f;
+        const int64_t base = ((int64_t)h * N + q) * D;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int d = 32 * dt + 8 * i + 4 * hf;
+                const float v0 = o[dt][4 * i] * inv, v1 = o[dt][4 * i + 1] * inv;
+                const float v2 = o[dt][4 * i + 2] * inv, v3 = o[dt][4 * i + 3] * inv;
+                if (a.out_bf16) {
+                    *reinterpret_cast<uint2*>(static_cast<uint16_t*>(a.out) + base + d) =
+                        make_uint2(pack_bf16x2(v0, v1), pack_bf16x2(v2, v3));
+                } else {
+                    *reinterpret_cast<float4*>(static_cast<float*>(a.out) + base + d) =
+                        make_float4(v0, v1, v2, v3);
+                }
+            }
+    }
+}
+
+template <int D, int G>
+hipError_t launch_d_g(const AttnParams& a, float c, hipStream_t st) {
+    const int64_t tiles = (a.N + kRows - 1) / kRows;
+    hipLaunchKernelGGL((k_attn_tile<D, G>), dim3((unsigned)(tiles * a.Hkv)), dim3(64 * G), 0, st, a, c);
+    return hipGetLastError();
+}
+
+template <int D>
+hipError_t launch_d(const AttnParams& a, float c, hipStream_t st) {
+    switch (a.G) {
+        case 1: return launch_d_g<D, 1>(a, c, st);
+        case 2: return launch_d_g<D, 2>(a, c, st);
+        case 3: return launch_d_g<D, 3>(a, c, st);
+        case 4: return launch_d_g<D, 4>(a, c, st);
+        case 5: return launch_d_g<D, 5>(a, c, st);
+        case 6: return launch_d_g<D, 6>(a, c, st);
+        case 7: return launch_d_g<D, 7>(a, c, st);
+        default: return launch_d_g<D, 8>(a, c, st);
+    }
+}
+
+}  // namespace
+
+hipError_t launch_attn_tile(const AttnParams& a, hipStream_t st) {
+    const float c = a.scale * 1.4426950408889634f;   // scores to the log2 domain
+    return a.D == 128 ? launch_d<128>(a, c, st) : launch_d<64>(a, c, st);
+}
+
+}  // namespace ris

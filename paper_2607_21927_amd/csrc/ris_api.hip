@@ -187,8 +187,11 @@ int ris_sparse_attn(const void* Q, const void* K, const void* V, const int64_t* 
     a.in_bf16 = d.dtype_in == RIS_BF16; a.out_bf16 = d.dtype_out == RIS_BF16;
     a.mode = d.mode; a.block = d.block; a.causal = d.causal;
     a.scale = d.scale > 0.0f ? d.scale : 1.0f / sqrtf((float)d.D);
-    if (d.algo == RIS_ATTN_TILE) return RIS_E_UNSUPPORTED;
-    return hip_status(ris::launch_attn_gather(a, static_cast<hipStream_t>(stream)));
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    // The tiled MFMA kernel needs bf16 operands; float32 inputs take the gather kernel.
+    if (d.algo == RIS_ATTN_TILE && !a.in_bf16) return RIS_E_UNSUPPORTED;
+    if (d.algo == RIS_ATTN_GATHER || !a.in_bf16) return hip_status(ris::launch_attn_gather(a, s));
+    return hip_status(ris::launch_attn_tile(a, s));
 }
 
 }  // extern "C"

@@ -45,5 +45,6 @@ struct AttnParams {
     float scale;
 };
 hipError_t launch_attn_gather(const AttnParams& a, hipStream_t st);
+hipError_t launch_attn_tile(const AttnParams& a, hipStream_t st);
 
 }  // namespace ris
