@@ -2,7 +2,8 @@
 
 One step = one layer of the hot path over resident synthetic inputs:
 restore Q and K from pristine copies (RoPE rotates in place), RoPE on Q and K,
-geometry (count pass, scan, fill pass of the CSR), sparse attention.  The
+geometry (the CSR of the seed-ensemble union, built in one pass into a
+col_idx sized from the closed-form bound), sparse attention.  The
 default workload is the Qwen2-1.5B-shaped layer at N = 65,536 tokens, 1%
 density, 70 seeds, YaRN x2 -- the configuration the headline metric names.
 
@@ -125,7 +126,7 @@ def run_gpu(w, layer, Q, K, V, steps, warmup, algo):
             ris.rope(k, rd)
         if record:
             ev[1].record()
-        ris.mask_build(desc, row_ptr)
+        # col_idx sized from the closed-form bound: one call builds the CSR.
         ris.mask_build(desc, row_ptr, col_idx, col_capacity=cap)
         if record:
             ev[2].record()

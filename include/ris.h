@@ -96,12 +96,15 @@ typedef struct {
  *   the row sizes (row_ptr[0] = 0, row_ptr[heads*N] = nnz).  The caller then
  *   reads row_ptr[heads*N] (8 bytes) to size col_idx, or sizes it with
  *   ris_mask_nnz_bound() and skips that read.
- * Fill phase (col_idx != NULL): row_ptr must hold the count phase's output
- *   for the same descriptor; writes col_idx[row_ptr[r] .. row_ptr[r+1]) for
- *   every row.  If col_capacity >= ris_mask_nnz_bound(desc) the call is fully
- *   asynchronous; otherwise it first reads row_ptr[heads*N] (synchronising
- *   the stream) and returns RIS_E_CAPACITY, writing nothing, when
- *   col_capacity < nnz.  Writes never leave col_idx[0 .. col_capacity).
+ One-pass build (col_idx != NULL, col_capacity >= ris_mask_nnz_bound(desc)):
+ *   row_ptr need not hold anything; the call writes both row_ptr and col_idx,
+ *   generating every row once, fully asynchronously.  This is the fast path.
+ * Fill phase (col_idx != NULL, smaller capacity): row_ptr must hold the
+ *   count phase's output for the same descriptor; the call first reads
+ *   row_ptr[heads*N] (synchronising the stream), returns RIS_E_CAPACITY,
+ *   writing nothing, when col_capacity < nnz, and otherwise writes
+ *   col_idx[row_ptr[r] .. row_ptr[r+1]) for every row.
+ * Writes never leave col_idx[0 .. col_capacity).
  * Requires Structural mode to be causal.
  */
 int ris_mask_build(const ris_mask_desc* desc, int64_t* row_ptr, int32_t* col_idx,

@@ -40,8 +40,13 @@ __device__ __forceinline__ uint4 select4(bool keep, uint4 v) {
     return keep ? v : make_uint4(0u, 0u, 0u, 0u);
 }
 
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+
+// Two floats -> packed bf16 pair, round to nearest even (v_cvt_pk_bf16_f32).
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-    return (uint32_t)f32_to_bf16(lo) | ((uint32_t)f32_to_bf16(hi) << 16);
+    const f32x2_t f = {lo, hi};
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(f, bf16x2_t));
 }
 
 template <int D, int G>
@@ -53,12 +58,15 @@ __global__ __launch_bounds__(64 * G) void k_attn_tile(AttnParams a, float c) {
     constexpr int RPW = (kRows + G - 1) / G;
     constexpr int KSTEPS = D / 16;
     constexpr int DT = D / 32;
+    constexpr int KTASK = kKeys * (D / 8);          // 16-byte pieces of a K block
+    constexpr int VTASK = (kKeys / 2) * (D / 8);    // (key pair, 8 dims) pieces of a V block
+    constexpr int KPT = (KTASK + NT - 1) / NT;      // per thread
+    constexpr int VPT = (VTASK + NT - 1) / NT;
     __shared__ __align__(16) uint16_t Ks[kKeys * KS];
     __shared__ __align__(16) uint16_t Vt[D * VS];
     __shared__ __align__(16) uint16_t tags[kRows * TS];
-    __shared__ int64_t rstart[kRows];
-    __shared__ int32_t rlen[kRows];
-    __shared__ int32_t rcur[kRows];
+    __shared__ int64_t rstart_s[kRows];
+    __shared__ int32_t rlen_s[kRows];
     __shared__ int32_t wcount[G];
     __shared__ int32_t kb_range[2];
 
@@ -83,18 +91,17 @@ __global__ __launch_bounds__(64 * G) void k_attn_tile(AttnParams a, float c) {
             s = a.row_ptr[g * N + q];
             L = a.row_ptr[g * N + q + 1] - s;
         }
-        rstart[tid] = s;
-        rlen[tid] = (int)L;
-        rcur[tid] = 0;
+        rstart_s[tid] = s;
+        rlen_s[tid] = (int)L;
     }
     __syncthreads();
     // Key-block range touched by any row: first and last entries of each row.
     if (w == 0) {
         int lo = 0x7FFFFFFF, hi = -1;
-        if (lane < kRows && rlen[lane] > 0) {
+        if (lane < kRows && rlen_s[lane] > 0) {
             const int64_t nb = (N - 1) / kKeys;
-            int64_t f = a.col_idx[rstart[lane]] / kKeys;
-            int64_t l = a.col_idx[rstart[lane] + rlen[lane] - 1] / kKeys;
+            int64_t f = a.col_idx[rstart_s[lane]] / kKeys;
+            int64_t l = a.col_idx[rstart_s[lane] + rlen_s[lane] - 1] / kKeys;
             f = f < 0 ? 0 : (f > nb ? nb : f);
             l = l < 0 ? 0 : (l > nb ? nb : l);
             lo = (int)f;
@@ -124,30 +131,74 @@ __global__ __launch_bounds__(64 * G) void k_attn_tile(AttnParams a, float c) {
         for (int r = 0; r < 16; ++r) o[dt][r] = 0.f;
     __syncthreads();
 
+    // Rows this wave turns into tags: r = w + G*i.
+    int64_t rst[RPW];
+    int rln[RPW], cur[RPW];
+#pragma unroll
+    for (int i = 0; i < RPW; ++i) {
+        const int r = w + G * i;
+        rst[i] = r < kRows ? rstart_s[r] : 0;
+        rln[i] = r < kRows ? rlen_s[r] : 0;
+        cur[i] = 0;
+    }
     const int kb_lo = kb_range[0], kb_hi = kb_range[1];
+
+    // ---- register staging of one block (K pieces, V pair pieces, CSR windows)
+    uint4 kreg[KPT], vreg[VPT][2];
+    int wreg[RPW];
+    auto load_block = [&](int kb) {
+        const int64_t k0 = (int64_t)kb * kKeys;
+#pragma unroll
+        for (int u = 0; u < KPT; ++u) {
+            const int e = tid + u * NT;
+            const int key = e / (D / 8), ch = e % (D / 8);
+            const int64_t j = min(k0 + key, N - 1);
+            kreg[u] = (KTASK % NT == 0 || e < KTASK)
+                          ? *reinterpret_cast<const uint4*>(Kg + j * D + ch * 8) : make_uint4(0, 0, 0, 0);
+        }
+#pragma unroll
+        for (int u = 0; u < VPT; ++u) {
+            const int e = tid + u * NT;
+            const int p = e % (kKeys / 2), ch = e / (kKeys / 2);
+            const int64_t j0 = min(k0 + 2 * p, N - 1), j1 = min(k0 + 2 * p + 1, N - 1);
+            const bool ok = VTASK % NT == 0 || e < VTASK;
+            vreg[u][0] = ok ? *reinterpret_cast<const uint4*>(Vg + j0 * D + ch * 8) : make_uint4(0, 0, 0, 0);
+            vreg[u][1] = ok ? *reinterpret_cast<const uint4*>(Vg + j1 * D + ch * 8) : make_uint4(0, 0, 0, 0);
+        }
+#pragma unroll
+        for (int i = 0; i < RPW; ++i)
+            wreg[i] = lane < rln[i] - cur[i] ? a.col_idx[rst[i] + cur[i] + lane] : -1;
+    };
+
+    if (kb_lo <= kb_hi) load_block(kb_lo);
     for (int kb = kb_lo; kb <= kb_hi; ++kb) {
         const int64_t k0 = (int64_t)kb * kKeys;
-        // ---- stage K (row-major) and V (transposed) for this block
-        for (int e = tid; e < kKeys * (D / 8); e += NT) {
-            const int key = e / (D / 8), ch = e % (D / 8);
-            const int64_t j = k0 + key;
-            const uint4 v = select4(j < N, *reinterpret_cast<const uint4*>(Kg + min(j, N - 1) * D + ch * 8));
-            *reinterpret_cast<uint4*>(&Ks[key * KS + ch * 8]) = v;
-        }
-        for (int e = tid; e < (kKeys / 2) * (D / 8); e += NT) {
-            const int p = e % (kKeys / 2), ch = e / (kKeys / 2);
-            const int64_t j0 = k0 + 2 * p;
-            const uint4 v0 = select4(j0 < N, *reinterpret_cast<const uint4*>(Vg + min(j0, N - 1) * D + ch * 8));
-            const uint4 v1 =
-                select4(j0 + 1 < N, *reinterpret_cast<const uint4*>(Vg + min(j0 + 1, N - 1) * D + ch * 8));
-            const uint32_t a0[4] = {v0.x, v0.y, v0.z, v0.w};
-            const uint32_t a1[4] = {v1.x, v1.y, v1.z, v1.w};
+        // ---- registers -> LDS: K row-major, V transposed (keys of a pair side by side)
 #pragma unroll
-            for (int k = 0; k < 4; ++k) {
-                *reinterpret_cast<uint32_t*>(&Vt[(ch * 8 + 2 * k) * VS + 2 * p]) =
-                    (a0[k] & 0xFFFFu) | (a1[k] << 16);
-                *reinterpret_cast<uint32_t*>(&Vt[(ch * 8 + 2 * k + 1) * VS + 2 * p]) =
-                    (a0[k] >> 16) | (a1[k] & 0xFFFF0000u);
+        for (int u = 0; u < KPT; ++u) {
+            const int e = tid + u * NT;
+            if (KTASK % NT == 0 || e < KTASK) {
+                const int key = e / (D / 8), ch = e % (D / 8);
+                const bool live = k0 + key < N;
+                *reinterpret_cast<uint4*>(&Ks[key * KS + ch * 8]) = select4(live, kreg[u]);
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < VPT; ++u) {
+            const int e = tid + u * NT;
+            if (VTASK % NT == 0 || e < VTASK) {
+                const int p = e % (kKeys / 2), ch = e / (kKeys / 2);
+                const uint4 v0 = select4(k0 + 2 * p < N, vreg[u][0]);
+                const uint4 v1 = select4(k0 + 2 * p + 1 < N, vreg[u][1]);
+                const uint32_t a0[4] = {v0.x, v0.y, v0.z, v0.w};
+                const uint32_t a1[4] = {v1.x, v1.y, v1.z, v1.w};
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    *reinterpret_cast<uint32_t*>(&Vt[(ch * 8 + 2 * k) * VS + 2 * p]) =
+                        __builtin_amdgcn_perm(a1[k], a0[k], 0x05040100u);
+                    *reinterpret_cast<uint32_t*>(&Vt[(ch * 8 + 2 * k + 1) * VS + 2 * p]) =
+                        __builtin_amdgcn_perm(a1[k], a0[k], 0x07060302u);
+                }
             }
         }
         // ---- tags: keys of this block present in each row's set
@@ -157,19 +208,19 @@ __global__ __launch_bounds__(64 * G) void k_attn_tile(AttnParams a, float c) {
         for (int i = 0; i < RPW; ++i) {
             const int r = w + G * i;
             if (r < kRows) {
-                const int cur = rcur[r], len = rlen[r];
-                int64_t col = -1;
-                if (lane < len - cur) col = a.col_idx[rstart[r] + cur + lane];
+                const int64_t col = wreg[i];
                 const bool inb = col >= k0 && col < k0 + kKeys && col < N;
                 const uint64_t bal = __ballot(inb);
                 if (inb) tags[r * TS + (int)(col - k0)] = tag;
                 const int cnt = __popcll(bal);
-                if (lane == 0) rcur[r] = cur + cnt;
+                cur[i] += cnt;
                 my_cnt += cnt;
             }
         }
         if (lane == 0) wcount[w] = my_cnt;
         __syncthreads();
+        // ---- next block's loads fly while this block computes
+        if (kb < kb_hi) load_block(kb + 1);
         int any = 0;
 #pragma unroll
         for (int i = 0; i < G; ++i) any += wcount[i];
@@ -209,7 +260,6 @@ __global__ __launch_bounds__(64 * G) void k_attn_tile(AttnParams a, float c) {
             const float m_new = fmaxf(m_run, mx);
             const float m_use = m_new == -INFINITY ? 0.f : m_new;
             const float mc = m_use * c;
-            const float corr = __builtin_amdgcn_exp2f(fmaf(m_run, c, -mc));
             float rs = 0.f;
 #pragma unroll
             for (int t = 0; t < 2; ++t)
@@ -220,12 +270,16 @@ __global__ __launch_bounds__(64 * G) void k_attn_tile(AttnParams a, float c) {
                     rs += p;
                 }
             rs += __shfl_xor(rs, 32);
-            l_run = l_run * corr + rs;
+            if (__ballot(m_new != m_run) != 0ull) {      // some query's max moved: rescale
+                const float corr = __builtin_amdgcn_exp2f(fmaf(m_run, c, -mc));
+                l_run *= corr;
+#pragma unroll
+                for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) o[dt][r] *= corr;
+            }
+            l_run += rs;
             m_run = m_new;
-#pragma unroll
-            for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-                for (int r = 0; r < 16; ++r) o[dt][r] *= corr;
             // ---- P^T as the B operand: k-step (t, u) holds keys
             // 32t+16u+4hf+{0..3} and 32t+16u+8+4hf+{0..3}
             bf16x8_t pb[2][2];

@@ -174,6 +174,123 @@ __global__ __launch_bounds__(kThreads) void k_mask_fill(MaskParams p, const int6
     }
 }
 
+// ---------------------------------------------------------------------------
+// One-pass build (count, scan and fill fused), used when col_idx is sized from
+// the closed-form bound.  Each workgroup takes a ticket -- rows are processed
+// in row order -- builds its row bitmap once, and finds its offset by a
+// decoupled look-back over its predecessors' status words, which live in
+// row_ptr itself: bits 61/62 flag "row size known" / "inclusive prefix
+// known".  A row publishes its size before looking back (64 predecessors per
+// step, one per lane), and a ticket is only
+// ever waited on by later tickets, whose workgroups started after it; so every
+// wait ends.  The spin is bounded anyway: past the bound the row is left
+// unwritten rather than risk a hang.  Status words are read and written with
+// relaxed agent-scope atomics: they carry the only data exchanged.
+constexpr int64_t kFlagAgg = 1ll << 61;
+constexpr int64_t kFlagInc = 1ll << 62;
+constexpr int64_t kValueMask = kFlagAgg - 1;
+constexpr uint32_t kSpinLimit = 1u << 24;
+
+__device__ __forceinline__ int64_t status_load(const int64_t* p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void status_store(int64_t* p, int64_t v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__global__ __launch_bounds__(kThreads) void k_mask_fused(MaskParams p, int64_t* row_ptr,
+                                                         int32_t* col_idx, int64_t capacity) {
+    extern __shared__ uint32_t smem[];
+    __shared__ uint32_t red[4];
+    __shared__ int64_t s_ticket, s_base;
+    uint32_t* rks = smem;
+    uint32_t* bits = smem + kSeedBatch * 6;
+    const int64_t R = (int64_t)p.heads * p.N;
+    if (threadIdx.x == 0) {
+        const int64_t t = (int64_t)atomicAdd(reinterpret_cast<unsigned long long*>(row_ptr), 1ull);
+        s_ticket = t;
+        // The last ticket is the last increment of row_ptr[0]: restore it to 0.
+        if (t == R - 1) status_store(row_ptr, 0);
+    }
+    __syncthreads();
+    const int64_t r = s_ticket;
+    const int h = (int)(r / p.N);
+    const int64_t q = r - (int64_t)h * p.N;
+    const RowGeom g = row_geometry(p, q);
+    build_row_bitmap(p, q, h, g, rks, bits);
+    const uint32_t W = (g.pool + 31u) >> 5;
+    uint32_t c = 0;
+    for (uint32_t w = threadIdx.x; w < W; w += kThreads) c += __popc(bits[w]);
+    const int64_t count = (int64_t)block_sum(c, red) + g.clique_len;
+
+    if (threadIdx.x < 64) {
+        // Wave-wide look-back: lane i reads the status of row j-1-i, so each
+        // step covers 64 predecessors.  The step ends at the nearest row whose
+        // inclusive prefix is known, once every row before it is ready.
+        const int lane = threadIdx.x;
+        if (lane == 0) status_store(&row_ptr[r + 1], kFlagAgg | count);
+        int64_t prefix = 0;
+        bool ok = true;
+        uint32_t spins = 0;
+        for (int64_t j = r; j > 0;) {
+            const int64_t idx = j - lane;                       // row idx-1's status
+            const int64_t v = idx > 0 ? status_load(&row_ptr[idx]) : kFlagInc;
+            const uint64_t inc = __ballot((v & kFlagInc) != 0);
+            const uint64_t ready = __ballot((v & (kFlagInc | kFlagAgg)) != 0);
+            const int first = inc ? (int)__ffsll((unsigned long long)inc) - 1 : 64;
+            const uint64_t need = first >= 63 ? ~0ull : ((1ull << (first + 1)) - 1ull);
+            if ((ready & need) != need) {
+                if (++spins > kSpinLimit) { ok = false; break; }
+                __builtin_amdgcn_s_sleep(1);
+                continue;
+            }
+            int64_t part = lane <= first ? (v & kValueMask) : 0;
+            for (int off = 32; off > 0; off >>= 1) part += __shfl_xor(part, off);
+            prefix += part;
+            if (first < 64) break;
+            j -= 64;
+        }
+        if (lane == 0) {
+            status_store(&row_ptr[r + 1], kFlagInc | (prefix + count));
+            s_base = ok ? prefix : -1;
+        }
+    }
+    __syncthreads();
+    const int64_t base = s_base;
+    if (base < 0 || base > capacity) return;
+    int64_t limit = count;
+    if (limit > capacity - base) limit = capacity - base;
+    int32_t* out = col_idx + base;
+    uint32_t done = 0;
+    for (uint32_t w0 = 0; w0 < W; w0 += kThreads) {
+        const uint32_t w = w0 + threadIdx.x;
+        uint32_t word = w < W ? bits[w] : 0u;
+        uint32_t total;
+        int64_t pos = done + block_exclusive_scan(__popc(word), red, &total);
+        while (word) {
+            const uint32_t b = __ffs(word) - 1u;
+            word &= word - 1u;
+            if (pos < limit) out[pos] = (int32_t)(w * 32u + b);
+            ++pos;
+        }
+        done += total;
+    }
+    for (uint32_t t = threadIdx.x; t < g.clique_len; t += kThreads) {
+        const int64_t pos = (int64_t)done + t;
+        if (pos < limit) out[pos] = (int32_t)(g.clique_start + t);
+    }
+}
+
+__global__ void k_fill_i64(int64_t* x, int64_t n, int64_t v) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) x[i] = v;
+}
+
+__global__ void k_strip_status(int64_t* row_ptr, int64_t n) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) row_ptr[i] &= kValueMask;
+}
+
 // In-place inclusive scan of row_ptr[1 .. R] (row sizes -> end offsets);
 // row_ptr[0] = 0.  One workgroup walks the array in coalesced chunks.
 constexpr int kScanThreads = 1024;
@@ -232,6 +349,21 @@ hipError_t launch_mask_count(const MaskParams& p, int64_t* row_ptr, hipStream_t 
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(k_scan_rows, dim3(1), dim3(kScanThreads), 0, st, row_ptr, rows);
+    return hipGetLastError();
+}
+
+hipError_t launch_mask_fused(const MaskParams& p, int64_t* row_ptr, int32_t* col_idx,
+                             int64_t capacity, hipStream_t st) {
+    const int64_t rows = (int64_t)p.heads * p.N;
+    const unsigned eb = (unsigned)((rows + 1 + 255) / 256);
+    hipLaunchKernelGGL(k_fill_i64, dim3(eb), dim3(256), 0, st, row_ptr, rows + 1, (int64_t)0);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_mask_fused, dim3((unsigned)rows), dim3(kThreads), mask_smem_bytes(p), st, p,
+                       row_ptr, col_idx, capacity);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_strip_status, dim3(eb), dim3(256), 0, st, row_ptr, rows + 1);
     return hipGetLastError();
 }
 

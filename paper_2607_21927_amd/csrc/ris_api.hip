@@ -105,7 +105,10 @@ int ris_mask_build(const ris_mask_desc* desc, int64_t* row_ptr, int32_t* col_idx
     hipStream_t s = static_cast<hipStream_t>(stream);
     if (!col_idx) return hip_status(ris::launch_mask_count(p, row_ptr, s));
     if (col_capacity < 0) return RIS_E_ARG;
-    if (col_capacity < nnz_bound(p)) {
+    // Capacity covers every possible row: one fused pass computes row_ptr too.
+    if (col_capacity >= nnz_bound(p))
+        return hip_status(ris::launch_mask_fused(p, row_ptr, col_idx, col_capacity, s));
+    {
         int64_t nnz = 0;
         const int64_t rows = (int64_t)p.heads * p.N;
         if (hipMemcpyAsync(&nnz, row_ptr + rows, sizeof(nnz), hipMemcpyDeviceToHost, s) != hipSuccess)

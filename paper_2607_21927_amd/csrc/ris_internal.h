@@ -20,6 +20,8 @@ struct MaskParams {
 };
 
 hipError_t launch_mask_count(const MaskParams& p, int64_t* row_ptr, hipStream_t st);
+hipError_t launch_mask_fused(const MaskParams& p, int64_t* row_ptr, int32_t* col_idx,
+                             int64_t capacity, hipStream_t st);
 hipError_t launch_mask_fill(const MaskParams& p, const int64_t* row_ptr, int32_t* col_idx,
                             int64_t capacity, hipStream_t st);
 

@@ -176,8 +176,12 @@ def build_csr(desc, device="cuda", stream=None, use_bound=False):
     """
     import torch
     row_ptr = torch.empty(desc.heads * desc.N + 1, dtype=torch.int64, device=device)
-    mask_build(desc, row_ptr, None, stream=stream)
-    cap = mask_nnz_bound(desc) if use_bound else int(row_ptr[-1].item())
+    if use_bound:
+        # Bound-sized col_idx: one fused call computes row_ptr and col_idx.
+        cap = mask_nnz_bound(desc)
+    else:
+        mask_build(desc, row_ptr, None, stream=stream)
+        cap = int(row_ptr[-1].item())
     col_idx = torch.empty(max(cap, 1), dtype=torch.int32, device=device)
     mask_build(desc, row_ptr, col_idx, col_capacity=cap, stream=stream)
     return row_ptr, col_idx

@@ -26,13 +26,16 @@ SMALL = [
 ]
 
 
+@pytest.mark.parametrize("fused", [False, True], ids=["two_phase", "one_pass"])
 @pytest.mark.parametrize("cfg", SMALL)
-def test_mask_bit_exact_small(cfg):
+def test_mask_bit_exact_small(cfg, fused):
+    """Both build paths: count + scan + fill (col_idx sized exactly) and the
+    one-pass build (col_idx sized from the closed-form bound)."""
     ris = need_gpu()
     mode, ppm, N, heads, S, seed, layer, causal, block = cfg
     sp = spec_of(mode, ppm, N, heads, S, seed, layer, causal, block)
-    say(f"mask parity {cfg}")
-    rp, ci = gpu_csr(ris, sp)
+    say(f"mask parity {cfg} fused={fused}")
+    rp, ci = gpu_csr(ris, sp, use_bound=fused)
     want_rp, want_ci = o_geo.build_csr(sp)
     rp = rp.cpu().numpy()
     assert np.array_equal(rp, want_rp)
