@@ -88,7 +88,8 @@ typedef struct {
 } ris_mask_desc;
 
 /*
- * Build the CSR of one layer's geometry, in two phases.
+ * Build the CSR of one layer's geometry: in one pass into a col_idx sized
+ * from ris_mask_nnz_bound(), or in two phases for an exactly sized col_idx.
  *
  * row_ptr: device int64[heads*N + 1].  col_idx: device int32[col_capacity].
  *
@@ -96,7 +97,7 @@ typedef struct {
  *   the row sizes (row_ptr[0] = 0, row_ptr[heads*N] = nnz).  The caller then
  *   reads row_ptr[heads*N] (8 bytes) to size col_idx, or sizes it with
  *   ris_mask_nnz_bound() and skips that read.
- One-pass build (col_idx != NULL, col_capacity >= ris_mask_nnz_bound(desc)):
+ * One-pass build (col_idx != NULL, col_capacity >= ris_mask_nnz_bound(desc)):
  *   row_ptr need not hold anything; the call writes both row_ptr and col_idx,
  *   generating every row once, fully asynchronously.  This is the fast path.
  * Fill phase (col_idx != NULL, smaller capacity): row_ptr must hold the
