@@ -25,6 +25,7 @@ sys.path.insert(0, ROOT)
 from synth import ROPE_NONE, STRUCTURAL, WORKLOADS, gaussian_qkv, needle_plan, plant_needles  # noqa: E402
 
 HBM_PEAK_GBS = 8000.0
+PROFILES = os.path.join(ROOT, "profiles")
 KV_PAIR_BYTES = {128: 2 * 128 * 2 + 4, 64: 2 * 64 * 2 + 4}   # K row + V row (bf16) + int32 index
 
 
@@ -158,6 +159,24 @@ def run_gpu(w, layer, Q, K, V, steps, warmup, algo):
                 ms_attn=t_attn / steps, nnz=nnz)
 
 
+def measured_traffic(workload, kernel_source):
+    """HBM bytes per launch of the attention kernel from the committed
+    rocprofv3 counter record, or None when no record exists for this
+    workload or the kernel source changed since the counters were taken."""
+    import hashlib
+    path = os.path.join(PROFILES, f"attn_tile_{workload}_traffic.txt")
+    if not os.path.exists(path):
+        return None
+    rec = dict(line.strip().split("=", 1) for line in open(path)
+               if "=" in line and not line.startswith("#"))
+    src = os.path.join(ROOT, rec.get("source", ""))
+    if not os.path.exists(src) or rec.get("source") != kernel_source:
+        return None
+    if hashlib.sha256(open(src, "rb").read()).hexdigest() != rec.get("source_sha256"):
+        return None
+    return float(rec["traffic_bytes"])
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -192,6 +211,8 @@ def main():
     causal_pairs = w.Hkv * w.N * (w.N + 1) / 2
     alg_bytes = g["nnz"] * KV_PAIR_BYTES[w.D]
     achieved = alg_bytes / (g["ms_attn"] * 1e-3) / 1e9
+    tiled = w.dtype == "bf16" and args.algo != 1
+    traffic = measured_traffic(w.name, "paper_2607_21927_amd/csrc/attn_tile.hip") if tiled else None
     res = {
         "metric": "attended (q,k) pairs/s (whole hot-path step: RoPE + geometry + attention)",
         "value": pairs / (g["ms_step"] * 1e-3),
@@ -217,8 +238,9 @@ def main():
         "union_fraction": g["nnz"] / causal_pairs,
         "hbm_gbs_attn": achieved,
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": None,
-                     "kernel": "sparse attention", "bytes_per_kv_pair": KV_PAIR_BYTES[w.D]},
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
+                     "kernel": "k_attn_tile" if tiled else "k_attn_gather",
+                     "bytes_per_kv_pair": KV_PAIR_BYTES[w.D]},
         "cpu_baseline": cpu,
     }
     print(json.dumps(res))
