@@ -20,7 +20,7 @@ namespace ris {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kSeedBatch = 64;   // round keys of this many seeds live in LDS at once
+constexpr int kSeedBatch = 256;  // round keys of this many seeds live in LDS at once
 
 struct RowGeom {
     uint32_t pool;          // draw pool [0, pool)
@@ -52,6 +52,15 @@ __device__ __forceinline__ RowGeom row_geometry(const MaskParams& p, int64_t q) 
     return g;
 }
 
+// Seed index s and draw index j of flat index idx = s * draws + j (idx < 2^24,
+// so the float quotient is off by at most one and is corrected).
+__device__ __forceinline__ void split_draw(uint32_t idx, uint32_t draws, float inv_draws, int& s, int& j) {
+    s = (int)((float)idx * inv_draws);
+    j = (int)idx - s * (int)draws;
+    if (j < 0) { --s; j += (int)draws; }
+    if (j >= (int)draws) { ++s; j -= (int)draws; }
+}
+
 // Fill `bits` (W words, already visible to the whole block) with the union of
 // every seed's draws for row (h, q).  Ends with a block barrier.
 __device__ void build_row_bitmap(const MaskParams& p, int64_t q, int h, const RowGeom& g,
@@ -65,9 +74,12 @@ __device__ void build_row_bitmap(const MaskParams& p, int64_t q, int h, const Ro
     }
     const FeistelDomain dom = make_domain(g.pool);
     const float inv_draws = 1.0f / (float)g.draws;
-    for (int s0 = 0; s0 < p.n_seeds; s0 += kSeedBatch) {
-        const int sb = min(kSeedBatch, p.n_seeds - s0);
+    // Batches keep the flat (seed, draw) index below 2^24 for the float split.
+    const int batch = (int)min((uint32_t)kSeedBatch, (1u << 24) / g.draws);
+    for (int s0 = 0; s0 < p.n_seeds; s0 += batch) {
+        const int sb = min(batch, p.n_seeds - s0);
         __syncthreads();   // bitmap cleared / previous batch's keys no longer read
+        // Round keys of the batch's seeds, one Philox evaluation per lane.
         for (int t = tid; t < sb; t += kThreads) {
             uint32_t rk[6];
             row_round_keys(p.seed + (uint64_t)(s0 + t), (uint64_t)q, (uint64_t)h, (uint64_t)p.layer, rk);
@@ -75,17 +87,38 @@ __device__ void build_row_bitmap(const MaskParams& p, int64_t q, int h, const Ro
             for (int e = 0; e < 6; ++e) rks[t * 6 + e] = rk[e];
         }
         __syncthreads();
-        const uint32_t total = (uint32_t)sb * g.draws;   // < 2^24: float index math is exact
-        for (uint32_t idx = tid; idx < total; idx += kThreads) {
-            int s = (int)((float)idx * inv_draws);
-            int j = (int)idx - s * (int)g.draws;
-            if (j < 0) { --s; j += (int)g.draws; }
-            if (j >= (int)g.draws) { ++s; j -= (int)g.draws; }
-            uint32_t rk[6];
+        // Each lane walks its draws one permutation step per iteration: a lane
+        // whose value lands in the pool emits it and starts its next draw at
+        // once, so cycle walks of different lengths do not hold the wave at
+        // the slowest lane.  Every walk ends within the domain size (the cycle
+        // through j < n returns to j); the step bound only makes that explicit.
+        const uint32_t total = (uint32_t)sb * g.draws;
+        uint32_t idx = tid;
+        uint32_t x = 0, steps = 0;
+        uint32_t rk[6];
+        if (idx < total) {
+            int s, j;
+            split_draw(idx, g.draws, inv_draws, s, j);
+            x = (uint32_t)j;
 #pragma unroll
             for (int e = 0; e < 6; ++e) rk[e] = rks[s * 6 + e];
-            const uint32_t x = permute((uint32_t)j, rk, dom);
-            atomicOr(&bits[x >> 5], 1u << (x & 31u));
+        }
+        while (idx < total) {
+            x = feistel6(x, rk, dom.half, dom.mask);
+            ++steps;
+            if (x < dom.n || steps >= dom.size) {
+                if (x >= dom.n) x = 0;
+                atomicOr(&bits[x >> 5], 1u << (x & 31u));
+                idx += kThreads;
+                steps = 0;
+                if (idx < total) {
+                    int s, j;
+                    split_draw(idx, g.draws, inv_draws, s, j);
+                    x = (uint32_t)j;
+#pragma unroll
+                    for (int e = 0; e < 6; ++e) rk[e] = rks[s * 6 + e];
+                }
+            }
         }
     }
     __syncthreads();
