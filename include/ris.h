@@ -170,7 +170,10 @@ typedef struct {
     int32_t mode;            /* ris_mode the CSR was built with                 */
     int32_t block;           /* its Structural block (as in ris_mask_desc)      */
     int32_t causal;          /* as in ris_mask_desc                             */
-    int32_t algo;            /* ris_attn_algo; AUTO picks per tile              */
+    int32_t algo;            /* ris_attn_algo: GATHER = per-row gather kernel;  */
+                             /* TILE = 32-row tiles on MFMA (bf16 only); AUTO  */
+                             /* = per 32-row tile, TILE when the tile's union  */
+                             /* density is >= 6%, GATHER otherwise             */
 } ris_attn_desc;
 
 /*

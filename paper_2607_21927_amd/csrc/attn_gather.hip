@@ -83,6 +83,7 @@ __global__ __launch_bounds__(64) void k_attn_gather(AttnParams a, float qscale) 
     const int64_t i = blockIdx.x;
     const int64_t q = N - 1 - i / a.Hkv;
     const int g = (int)(i % a.Hkv);
+    if (tile_is_dense(a, g, q - q % kTileRows)) return;   // that tile runs on the tiled kernel
     const int64_t r = (int64_t)g * N + q;
     const int64_t start = a.row_ptr[r];
     const int64_t L = a.row_ptr[r + 1] - start;

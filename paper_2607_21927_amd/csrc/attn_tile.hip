@@ -28,7 +28,7 @@ namespace {
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
-constexpr int kRows = 32;   // query rows per tile (MFMA N)
+constexpr int kRows = kTileRows;   // query rows per tile (MFMA N)
 constexpr int kKeys = 64;   // keys per block
 
 __device__ __forceinline__ bf16x8_t as_bf16x8(uint4 v) {
@@ -81,6 +81,7 @@ __global__ __launch_bounds__(64 * G) void k_attn_tile(AttnParams a, float c) {
     const int h = g * G + w;
     const uint16_t* Kg = static_cast<const uint16_t*>(a.K) + (int64_t)g * N * D;
     const uint16_t* Vg = static_cast<const uint16_t*>(a.V) + (int64_t)g * N * D;
+    if (!tile_is_dense(a, g, q0)) return;   // a sparse tile belongs to the gather kernel
 
     // ---- per-row CSR extents, tags cleared
     for (int i = tid; i < kRows * TS; i += NT) tags[i] = 0;

@@ -71,6 +71,8 @@ int64_t nnz_bound(const MaskParams& p) {
 
 int hip_status(hipError_t e) { return e == hipSuccess ? RIS_OK : RIS_E_HIP; }
 
+constexpr float kAutoDensity = 0.06f;
+
 }  // namespace
 
 extern "C" {
@@ -193,8 +195,21 @@ int ris_sparse_attn(const void* Q, const void* K, const void* V, const int64_t* 
     hipStream_t s = static_cast<hipStream_t>(stream);
     // The tiled MFMA kernel needs bf16 operands; float32 inputs take the gather kernel.
     if (d.algo == RIS_ATTN_TILE && !a.in_bf16) return RIS_E_UNSUPPORTED;
-    if (d.algo == RIS_ATTN_GATHER || !a.in_bf16) return hip_status(ris::launch_attn_gather(a, s));
-    return hip_status(ris::launch_attn_tile(a, s));
+    if (d.algo == RIS_ATTN_GATHER || !a.in_bf16) {
+        a.tau = INFINITY;                       // every tile to the gather kernel
+        return hip_status(ris::launch_attn_gather(a, s));
+    }
+    if (d.algo == RIS_ATTN_TILE) {
+        a.tau = -1.0f;                          // every tile to the tiled kernel
+        return hip_status(ris::launch_attn_tile(a, s));
+    }
+    // AUTO: per 32-row tile by union density.  The tiled kernel's cost grows
+    // with the key span, the gather kernel's with the entries; on MI355X they
+    // cross near 6% (Qwen2 shape, measured).
+    a.tau = kAutoDensity;
+    const int st = hip_status(ris::launch_attn_tile(a, s));
+    if (st != RIS_OK) return st;
+    return hip_status(ris::launch_attn_gather(a, s));
 }
 
 }  // extern "C"

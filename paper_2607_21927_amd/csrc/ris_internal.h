@@ -45,7 +45,22 @@ struct AttnParams {
     int32_t in_bf16, out_bf16;
     int32_t mode, block, causal;
     float scale;
+    // Per 32-row tile, the tiled kernel takes tiles whose union density
+    // (tile nnz / (rows x key span)) is >= tau and the gather kernel the rest.
+    float tau;
 };
+
+// Rows per tile of the tiled kernel; also the unit of the dispatch decision.
+constexpr int kTileRows = 32;
+
+// Density decision for the tile of rows [q0, q0 + kTileRows) of KV head g:
+// two reads of row_ptr.  The key span is [0, last row] (causal) or [0, N).
+__device__ __forceinline__ bool tile_is_dense(const AttnParams& a, int g, int64_t q0) {
+    const int64_t q1 = q0 + kTileRows < a.N ? q0 + kTileRows : a.N;
+    const int64_t nnz = a.row_ptr[g * a.N + q1] - a.row_ptr[g * a.N + q0];
+    const double span = a.causal ? (double)q1 : (double)a.N;
+    return (double)nnz >= (double)a.tau * (double)(q1 - q0) * span;
+}
 hipError_t launch_attn_gather(const AttnParams& a, hipStream_t st);
 hipError_t launch_attn_tile(const AttnParams& a, hipStream_t st);
 

@@ -46,6 +46,8 @@ def run_case(Hq, Hkv, N, D, mode, ppm, S, block=0, dtype_in="bf16", dtype_out="f
 
 
 def tight_tol(algo, V_max):
+    """Derived bound: gather 2e-4; tiled (and AUTO, which may use it) adds
+    the bf16 rounding of the softmax weights, 2^-9 max|V|."""
     return 2e-4 if algo == 1 else 2.0**-9 * V_max + 2e-4
 
 
@@ -65,13 +67,15 @@ CASES = [
 ]
 
 
-@pytest.mark.parametrize("algo", [1, 2], ids=["gather", "tile"])
+@pytest.mark.parametrize("algo", [1, 2, 0], ids=["gather", "tile", "auto"])
 @pytest.mark.parametrize("case", CASES)
 def test_attention_matches_oracle(case, algo):
     Hq, Hkv, N, D, mode, ppm, S, block, din, dout = case[:10]
     causal = case[10] if len(case) > 10 else 1
     if din == "f32" and algo == 2:
         pytest.skip("the tiled MFMA kernel takes bf16 operands")
+    if din == "f32" and algo == 0:
+        algo = 1                     # AUTO takes the gather kernel for float32
     say(f"attention parity {case} algo {algo}")
     got, want, _ = run_case(Hq, Hkv, N, D, mode, ppm, S, block, din, dout, causal, algo=algo)
     err = float(np.abs(got - want).max())
@@ -128,3 +132,26 @@ def test_tile_kernel_paper_block_rule_and_sparse_rows():
     assert float(np.abs(got - want).max()) <= tight_tol(2, 5.5)
     got, want, _ = run_case(12, 2, 3000, 128, 0, 1_000, 1, algo=2)
     assert float(np.abs(got - want).max()) <= tight_tol(2, 5.5)
+
+
+def test_auto_dispatch_mixed_density():
+    """AUTO splits by 32-row tile: at 1% x 6 seeds the first tiles (k >= 1 on
+    a short prefix) are dense and go to the tiled kernel, later tiles (~5.9%
+    union) to the gather kernel; the result is the oracle's either way, and
+    each tile's rows equal the output of the kernel its density selects."""
+    from oracle import geometry as o_geo
+    N, ppm, S = 2500, 10_000, 6
+    got, want, _ = run_case(12, 2, N, 128, 0, ppm, S, algo=0)
+    assert float(np.abs(got - want).max()) <= tight_tol(0, 5.5)
+    got_g, _, _ = run_case(12, 2, N, 128, 0, ppm, S, algo=1)
+    got_t, _, _ = run_case(12, 2, N, 128, 0, ppm, S, algo=2)
+    tau = float(np.float32(0.06))            # the library's threshold, as float32
+    sp = spec_of(0, ppm, N, 2, S)
+    dense = np.zeros(N, dtype=bool)
+    for q0 in range(0, N, 32):
+        q1 = min(N, q0 + 32)
+        nnz = sum(len(x) for x in o_geo.row_sets(sp, 0, np.arange(q0, q1)))
+        dense[q0:q1] = nnz >= tau * (q1 - q0) * q1
+    assert dense.any() and (~dense).any()
+    assert np.array_equal(got[:6][:, ~dense], got_g[:6][:, ~dense])
+    assert np.array_equal(got[:6][:, dense], got_t[:6][:, dense])
