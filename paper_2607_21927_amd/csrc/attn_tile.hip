@@ -27,12 +27,24 @@ namespace {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 constexpr int kRows = kTileRows;   // query rows per tile (MFMA N)
 constexpr int kKeys = 64;   // keys per block
 
 __device__ __forceinline__ bf16x8_t as_bf16x8(uint4 v) {
     return __builtin_bit_cast(bf16x8_t, v);
+}
+
+// max / sum of x over this lane and the lane 32 away (v_permlane32_swap:
+// with both operands x, the two results hold x at lanes l and l^32).
+__device__ __forceinline__ float pair_max32(float x) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float pair_sum32(float x) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
 // v if keep, else zeros (the load itself always reads a valid address).
@@ -145,33 +157,38 @@ __global__ __launch_bounds__(64 * G) void k_attn_tile(AttnParams a, float c) {
     const int kb_lo = kb_range[0], kb_hi = kb_range[1];
 
     // ---- register staging of one block (K pieces, V pair pieces, CSR windows)
-    uint4 kreg[KPT], vreg[VPT][2];
+    u32x4_t kreg[KPT], vreg[VPT][2];
     int wreg[RPW];
-    auto load_block = [&](int kb) {
-        const int64_t k0 = (int64_t)kb * kKeys;
+    auto load_kv = [&](int kb) {
+        const int k0 = kb * kKeys;
 #pragma unroll
         for (int u = 0; u < KPT; ++u) {
             const int e = tid + u * NT;
             const int key = e / (D / 8), ch = e % (D / 8);
-            const int64_t j = min(k0 + key, N - 1);
-            kreg[u] = (KTASK % NT == 0 || e < KTASK)
-                          ? *reinterpret_cast<const uint4*>(Kg + j * D + ch * 8) : make_uint4(0, 0, 0, 0);
+            const int64_t j = min(k0 + key, (int)N - 1);   // rows past N are masked out
+            if (KTASK % NT == 0 || e < KTASK) kreg[u] = *reinterpret_cast<const u32x4_t*>(Kg + j * D + ch * 8);
         }
 #pragma unroll
         for (int u = 0; u < VPT; ++u) {
             const int e = tid + u * NT;
             const int p = e % (kKeys / 2), ch = e / (kKeys / 2);
-            const int64_t j0 = min(k0 + 2 * p, N - 1), j1 = min(k0 + 2 * p + 1, N - 1);
-            const bool ok = VTASK % NT == 0 || e < VTASK;
-            vreg[u][0] = ok ? *reinterpret_cast<const uint4*>(Vg + j0 * D + ch * 8) : make_uint4(0, 0, 0, 0);
-            vreg[u][1] = ok ? *reinterpret_cast<const uint4*>(Vg + j1 * D + ch * 8) : make_uint4(0, 0, 0, 0);
+            const int64_t j0 = min(k0 + 2 * p, (int)N - 1), j1 = min(k0 + 2 * p + 1, (int)N - 1);
+            if (VTASK % NT == 0 || e < VTASK) {
+                vreg[u][0] = *reinterpret_cast<const u32x4_t*>(Vg + j0 * D + ch * 8);
+                vreg[u][1] = *reinterpret_cast<const u32x4_t*>(Vg + j1 * D + ch * 8);
+            }
         }
+    };
+    auto load_windows = [&]() {
 #pragma unroll
         for (int i = 0; i < RPW; ++i)
             wreg[i] = lane < rln[i] - cur[i] ? a.col_idx[rst[i] + cur[i] + lane] : -1;
     };
 
-    if (kb_lo <= kb_hi) load_block(kb_lo);
+    if (kb_lo <= kb_hi) {
+        load_kv(kb_lo);
+        load_windows();
+    }
     for (int kb = kb_lo; kb <= kb_hi; ++kb) {
         const int64_t k0 = (int64_t)kb * kKeys;
         // ---- registers -> LDS: K row-major, V transposed (keys of a pair side by side)
@@ -180,8 +197,7 @@ __global__ __launch_bounds__(64 * G) void k_attn_tile(AttnParams a, float c) {
             const int e = tid + u * NT;
             if (KTASK % NT == 0 || e < KTASK) {
                 const int key = e / (D / 8), ch = e % (D / 8);
-                const bool live = k0 + key < N;
-                *reinterpret_cast<uint4*>(&Ks[key * KS + ch * 8]) = select4(live, kreg[u]);
+                *reinterpret_cast<u32x4_t*>(&Ks[key * KS + ch * 8]) = kreg[u];   // rows past N: masked
             }
         }
 #pragma unroll
@@ -189,19 +205,22 @@ __global__ __launch_bounds__(64 * G) void k_attn_tile(AttnParams a, float c) {
             const int e = tid + u * NT;
             if (VTASK % NT == 0 || e < VTASK) {
                 const int p = e % (kKeys / 2), ch = e / (kKeys / 2);
-                const uint4 v0 = select4(k0 + 2 * p < N, vreg[u][0]);
-                const uint4 v1 = select4(k0 + 2 * p + 1 < N, vreg[u][1]);
-                const uint32_t a0[4] = {v0.x, v0.y, v0.z, v0.w};
-                const uint32_t a1[4] = {v1.x, v1.y, v1.z, v1.w};
+                u32x4_t v0 = vreg[u][0], v1 = vreg[u][1];
+                if (k0 + kKeys > N) {                       // V rows past N read as zeros
+                    if (k0 + 2 * p >= N) v0 = u32x4_t{0u, 0u, 0u, 0u};
+                    if (k0 + 2 * p + 1 >= N) v1 = u32x4_t{0u, 0u, 0u, 0u};
+                }
 #pragma unroll
                 for (int k = 0; k < 4; ++k) {
                     *reinterpret_cast<uint32_t*>(&Vt[(ch * 8 + 2 * k) * VS + 2 * p]) =
-                        __builtin_amdgcn_perm(a1[k], a0[k], 0x05040100u);
+                        __builtin_amdgcn_perm(v1[k], v0[k], 0x05040100u);
                     *reinterpret_cast<uint32_t*>(&Vt[(ch * 8 + 2 * k + 1) * VS + 2 * p]) =
-                        __builtin_amdgcn_perm(a1[k], a0[k], 0x07060302u);
+                        __builtin_amdgcn_perm(v1[k], v0[k], 0x07060302u);
                 }
             }
         }
+        // ---- the next block's K/V loads fly from here until its staging
+        if (kb < kb_hi) load_kv(kb + 1);
         // ---- tags: keys of this block present in each row's set
         const uint16_t tag = (uint16_t)(kb + 1);
         int my_cnt = 0;
@@ -209,10 +228,11 @@ __global__ __launch_bounds__(64 * G) void k_attn_tile(AttnParams a, float c) {
         for (int i = 0; i < RPW; ++i) {
             const int r = w + G * i;
             if (r < kRows) {
-                const int64_t col = wreg[i];
-                const bool inb = col >= k0 && col < k0 + kKeys && col < N;
+                const int col = wreg[i];
+                const int k0i = kb * kKeys;
+                const bool inb = col >= k0i && col < k0i + kKeys && col < (int)N;
                 const uint64_t bal = __ballot(inb);
-                if (inb) tags[r * TS + (int)(col - k0)] = tag;
+                if (inb) tags[r * TS + (col - k0i)] = tag;
                 const int cnt = __popcll(bal);
                 cur[i] += cnt;
                 my_cnt += cnt;
@@ -220,8 +240,8 @@ __global__ __launch_bounds__(64 * G) void k_attn_tile(AttnParams a, float c) {
         }
         if (lane == 0) wcount[w] = my_cnt;
         __syncthreads();
-        // ---- next block's loads fly while this block computes
-        if (kb < kb_hi) load_block(kb + 1);
+        // ---- next block's CSR windows (cursors are now past this block)
+        if (kb < kb_hi) load_windows();
         int any = 0;
 #pragma unroll
         for (int i = 0; i < G; ++i) any += wcount[i];
@@ -257,7 +277,7 @@ __global__ __launch_bounds__(64 * G) void k_attn_tile(AttnParams a, float c) {
                     }
                 }
             }
-            mx = fmaxf(mx, __shfl_xor(mx, 32));
+            mx = pair_max32(mx);
             const float m_new = fmaxf(m_run, mx);
             const float m_use = m_new == -INFINITY ? 0.f : m_new;
             const float mc = m_use * c;
@@ -270,7 +290,7 @@ __global__ __launch_bounds__(64 * G) void k_attn_tile(AttnParams a, float c) {
                     st[t][r] = p;
                     rs += p;
                 }
-            rs += __shfl_xor(rs, 32);
+            rs = pair_sum32(rs);
             if (__ballot(m_new != m_run) != 0ull) {      // some query's max moved: rescale
                 const float corr = __builtin_amdgcn_exp2f(fmaf(m_run, c, -mc));
                 l_run *= corr;
