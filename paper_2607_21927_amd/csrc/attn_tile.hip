@@ -28,6 +28,17 @@ namespace {
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+typedef short s16x4_t __attribute__((ext_vector_type(4)));
+
+// LDS transpose read (ds_read_b64_tr_b16).  Within each group of 16 lanes,
+// lane i receives element i mod 4 of what lanes 4e + i/4 (e = 0..3) address;
+// so if lane j addresses 4 consecutive dims of key row j/4 at dim offset
+// 4 (j mod 4), lane i gets dim i of four consecutive keys.
+__device__ __forceinline__ uint2 lds_read_tr16(const uint16_t* p) {
+    typedef __attribute__((address_space(3))) s16x4_t lds_s16x4;
+    const s16x4_t v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(p));
+    return __builtin_bit_cast(uint2, v);
+}
 
 constexpr int kRows = kTileRows;   // query rows per tile (MFMA N)
 constexpr int kKeys = 64;   // keys per block
@@ -65,17 +76,18 @@ template <int D, int G>
 __global__ __launch_bounds__(64 * G) void k_attn_tile(AttnParams a, float c) {
     constexpr int NT = 64 * G;
     constexpr int KS = D + 8;          // K row stride in LDS (bf16 elements)
-    constexpr int VS = kKeys + 4;      // V^T row stride
+    constexpr int VS = D + 16;         // V row stride: the 4 rows a 16-lane transpose read
+                                       // touches start 8 banks apart
     constexpr int TS = kKeys + 4;      // tag row stride
     constexpr int RPW = (kRows + G - 1) / G;
     constexpr int KSTEPS = D / 16;
     constexpr int DT = D / 32;
     constexpr int KTASK = kKeys * (D / 8);          // 16-byte pieces of a K block
-    constexpr int VTASK = (kKeys / 2) * (D / 8);    // (key pair, 8 dims) pieces of a V block
+    constexpr int VTASK = kKeys * (D / 8);          // 16-byte pieces of a V block
     constexpr int KPT = (KTASK + NT - 1) / NT;      // per thread
     constexpr int VPT = (VTASK + NT - 1) / NT;
     __shared__ __align__(16) uint16_t Ks[kKeys * KS];
-    __shared__ __align__(16) uint16_t Vt[D * VS];
+    __shared__ __align__(16) uint16_t Vs[kKeys * VS];
     __shared__ __align__(16) uint16_t tags[kRows * TS];
     __shared__ int64_t rstart_s[kRows];
     __shared__ int32_t rlen_s[kRows];
@@ -157,7 +169,7 @@ __global__ __launch_bounds__(64 * G) void k_attn_tile(AttnParams a, float c) {
     const int kb_lo = kb_range[0], kb_hi = kb_range[1];
 
     // ---- register staging of one block (K pieces, V pair pieces, CSR windows)
-    u32x4_t kreg[KPT], vreg[VPT][2];
+    u32x4_t kreg[KPT], vreg[VPT];
     int wreg[RPW];
     auto load_kv = [&](int kb) {
         const int k0 = kb * kKeys;
@@ -171,12 +183,9 @@ __global__ __launch_bounds__(64 * G) void k_attn_tile(AttnParams a, float c) {
 #pragma unroll
         for (int u = 0; u < VPT; ++u) {
             const int e = tid + u * NT;
-            const int p = e % (kKeys / 2), ch = e / (kKeys / 2);
-            const int64_t j0 = min(k0 + 2 * p, (int)N - 1), j1 = min(k0 + 2 * p + 1, (int)N - 1);
-            if (VTASK % NT == 0 || e < VTASK) {
-                vreg[u][0] = *reinterpret_cast<const u32x4_t*>(Vg + j0 * D + ch * 8);
-                vreg[u][1] = *reinterpret_cast<const u32x4_t*>(Vg + j1 * D + ch * 8);
-            }
+            const int key = e / (D / 8), ch = e % (D / 8);
+            const int64_t j = min(k0 + key, (int)N - 1);
+            if (VTASK % NT == 0 || e < VTASK) vreg[u] = *reinterpret_cast<const u32x4_t*>(Vg + j * D + ch * 8);
         }
     };
     auto load_windows = [&]() {
@@ -204,19 +213,10 @@ __global__ __launch_bounds__(64 * G) void k_attn_tile(AttnParams a, float c) {
         for (int u = 0; u < VPT; ++u) {
             const int e = tid + u * NT;
             if (VTASK % NT == 0 || e < VTASK) {
-                const int p = e % (kKeys / 2), ch = e / (kKeys / 2);
-                u32x4_t v0 = vreg[u][0], v1 = vreg[u][1];
-                if (k0 + kKeys > N) {                       // V rows past N read as zeros
-                    if (k0 + 2 * p >= N) v0 = u32x4_t{0u, 0u, 0u, 0u};
-                    if (k0 + 2 * p + 1 >= N) v1 = u32x4_t{0u, 0u, 0u, 0u};
-                }
-#pragma unroll
-                for (int k = 0; k < 4; ++k) {
-                    *reinterpret_cast<uint32_t*>(&Vt[(ch * 8 + 2 * k) * VS + 2 * p]) =
-                        __builtin_amdgcn_perm(v1[k], v0[k], 0x05040100u);
-                    *reinterpret_cast<uint32_t*>(&Vt[(ch * 8 + 2 * k + 1) * VS + 2 * p]) =
-                        __builtin_amdgcn_perm(v1[k], v0[k], 0x07060302u);
-                }
+                const int key = e / (D / 8), ch = e % (D / 8);
+                u32x4_t v = vreg[u];
+                if (k0 + key >= N) v = u32x4_t{0u, 0u, 0u, 0u};   // V rows past N read as zeros
+                *reinterpret_cast<u32x4_t*>(&Vs[key * VS + ch * 8]) = v;
             }
         }
         // ---- the next block's K/V loads fly from here until its staging
@@ -322,9 +322,12 @@ __global__ __launch_bounds__(64 * G) void k_attn_tile(AttnParams a, float c) {
                 for (int t = 0; t < 2; ++t)
 #pragma unroll
                     for (int u = 0; u < 2; ++u) {
-                        const uint16_t* vrow = &Vt[(32 * dt + n) * VS + 32 * t + 16 * u + 4 * hf];
-                        const uint2 lo = *reinterpret_cast<const uint2*>(vrow);
-                        const uint2 hi = *reinterpret_cast<const uint2*>(vrow + 8);
+                        // lane i of each 16-lane group: dim 32dt + 16*((lane/16)&1) + i,
+                        // keys 32t+16u+4hf+{0..3} (lo) and +8 (hi), as P^T holds them
+                        const uint16_t* vp = &Vs[(32 * t + 16 * u + 4 * hf + ((lane & 15) >> 2)) * VS +
+                                                 32 * dt + 16 * ((lane >> 4) & 1) + 4 * (lane & 3)];
+                        const uint2 lo = lds_read_tr16(vp);
+                        const uint2 hi = lds_read_tr16(vp + 8 * VS);
                         const bf16x8_t av = as_bf16x8(make_uint4(lo.x, lo.y, hi.x, hi.y));
                         o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pb[t][u], o[dt], 0, 0, 0);
                     }
