@@ -25,6 +25,7 @@ sys.path.insert(0, ROOT)
 from synth import ROPE_NONE, STRUCTURAL, WORKLOADS, gaussian_qkv, needle_plan, plant_needles  # noqa: E402
 
 HBM_PEAK_GBS = 8000.0
+MFMA_BF16_PEAK_TFS = 2500.0          # dense bf16 matrix peak of MI355X
 PROFILES = os.path.join(ROOT, "profiles")
 KV_PAIR_BYTES = {128: 2 * 128 * 2 + 4, 64: 2 * 64 * 2 + 4}   # K row + V row (bf16) + int32 index
 
@@ -241,6 +242,16 @@ def main():
                      "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
                      "kernel": "k_attn_tile" if tiled else "k_attn_gather",
                      "bytes_per_kv_pair": KV_PAIR_BYTES[w.D]},
+        # The tiled kernel reads each K/V block once per 32 rows, so its real
+        # bound is matrix/vector work: the method's flops (4 D G per kv-pair:
+        # QK^T and PV for the G heads) against the dense bf16 MFMA peak, and
+        # the masked-dense flops it actually issues over every touched block.
+        "roofline_mfma": {
+            "bound": "mfma", "unit": "TFLOP/s", "peak": MFMA_BF16_PEAK_TFS,
+            "achieved": pairs * 4 * w.D / (g["ms_attn"] * 1e-3) / 1e12,
+            "frac": pairs * 4 * w.D / (g["ms_attn"] * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFS,
+            "issued_dense_masked_tflops": (w.Hq * causal_pairs / w.Hkv * 4 * w.D
+                                           / (g["ms_attn"] * 1e-3) / 1e12) if tiled else None},
         "cpu_baseline": cpu,
     }
     print(json.dumps(res))
