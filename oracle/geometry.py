@@ -34,6 +34,12 @@ Readings taken where the paper is silent (each also listed in the design notes):
    hash, so layers get distinct sets.
 6. The hash is keyed by the KV head, so all query heads of a GQA group share
    one set.
+7. The full RIS geometry (Methods, "Ensemble Stochastic Projection and
+   Retrieval Coverage") also holds a dense local sliding window of L tokens
+   and a global anchor over the initial tokens.  Reading: both join the same
+   union -- window ``[max(0, q - L + 1), q]``, anchor ``[0, min(A, q + 1))`` --
+   on top of the ensemble's draws, whose counts are unchanged; the paper does
+   not give A (``anchor = 0`` and ``window = 0`` leave them out).  Causal only.
 """
 
 from dataclasses import dataclass
@@ -59,6 +65,8 @@ class MaskSpec:
     heads: int          # KV heads
     causal: int = 1
     block: int = 0      # Structural B; 0 = the paper's rule
+    window: int = 0     # dense local window L (0 = none)
+    anchor: int = 0     # initial-token anchor A (0 = none)
 
 
 def row_count(ppm, n):
@@ -97,15 +105,27 @@ def seed_draws(spec, kv_head, q, s):
     return prp.draw(int(kk[0]), int(n[0]), rk).astype(np.int64)
 
 
+def fixed_ranges(spec, q):
+    """The row's deterministic ranges: Structural clique, local window and
+    initial-token anchor (as (lo, hi) half-open intervals)."""
+    out = []
+    if spec.mode == STRUCTURAL:
+        start = int(_pool_and_draws(spec, np.array([q]))[2][0])
+        out.append((start, q + 1))
+    if spec.window > 0:
+        out.append((max(0, q - spec.window + 1), q + 1))
+    if spec.anchor > 0:
+        out.append((0, min(spec.anchor, q + 1)))
+    return out
+
+
 def row_set(spec, kv_head, q):
     """I(kv_head, q): sorted, unique union of every seed's set for one row.
 
     Written as the plain definition (one seed at a time, then ``unique``).
     """
     parts = [seed_draws(spec, kv_head, q, s) for s in range(spec.n_seeds)]
-    if spec.mode == STRUCTURAL:
-        start = int(_pool_and_draws(spec, np.array([q]))[2][0])
-        parts.append(np.arange(start, q + 1, dtype=np.int64))
+    parts += [np.arange(lo, hi, dtype=np.int64) for lo, hi in fixed_ranges(spec, q)]
     return np.unique(np.concatenate(parts)) if parts else np.zeros(0, np.int64)
 
 
@@ -129,12 +149,13 @@ def row_sets(spec, kv_head, qs):
     j = within % np.repeat(np.maximum(kk, 1), per_row)
     keys = prp.permute(j.astype(np.uint64), rk[ri, si], n[ri].astype(np.uint64)).astype(np.int64)
     stride = np.int64(spec.N + 1)
-    if spec.mode == STRUCTURAL:
-        cl = qs - start + 1
-        ci = np.repeat(np.arange(len(qs)), cl)
-        cv = np.arange(int(cl.sum())) - np.repeat(np.cumsum(cl) - cl, cl) + np.repeat(start, cl)
-        ri = np.concatenate([ri, ci])
-        keys = np.concatenate([keys, cv])
+    ranges_r, ranges_v = [ri], [keys]
+    for i, q in enumerate(qs):
+        for lo, hi in fixed_ranges(spec, int(q)):
+            ranges_r.append(np.full(hi - lo, i, dtype=np.int64))
+            ranges_v.append(np.arange(lo, hi, dtype=np.int64))
+    ri = np.concatenate(ranges_r)
+    keys = np.concatenate(ranges_v)
     u = np.unique(ri.astype(np.int64) * stride + keys)
     rows = u // stride
     vals = u % stride
@@ -161,10 +182,14 @@ def build_csr(spec, batch=256):
 
 def nnz_upper_bound(spec):
     """Closed-form upper bound on nnz: each row's union is at most
-    min(pool, S * draws) plus its clique."""
+    min(pool, S * draws) plus its clique, window and anchor, and never more
+    than the row's key span."""
     q = np.arange(spec.N, dtype=np.int64)
     n, kk, start = _pool_and_draws(spec, q)
     per = np.minimum(n, spec.n_seeds * kk)
     if spec.mode == STRUCTURAL:
         per = per + (q - start + 1)
+    if spec.window > 0 or spec.anchor > 0:
+        per = per + np.minimum(spec.window, q + 1) + np.minimum(spec.anchor, q + 1)
+        per = np.minimum(per, q + 1)
     return int(per.sum()) * spec.heads

@@ -162,3 +162,30 @@ def test_nnz_bound_is_an_upper_bound():
         assert geo.nnz_upper_bound(sp) >= row_ptr[-1]
     sp = spec(density_ppm=100_000, N=512)
     assert geo.nnz_upper_bound(sp) == 13_162      # single seed: exact
+
+
+def test_window_and_anchor_ranges():
+    """Full RIS geometry: every row holds its local window and the anchor
+    prefix on top of the draws; with a 1-key draw the row is exactly their
+    union; ppm = 10^6 still gives the causal triangle."""
+    for mode in (geo.STOCHASTIC, geo.STRUCTURAL):
+        sp = spec(mode=mode, density_ppm=20_000, N=700, n_seeds=3, window=50, anchor=7, block=64)
+        row_ptr, col_idx = geo.build_csr(sp)
+        check_csr(sp, row_ptr, col_idx)
+        for q in range(sp.N):
+            row = col_idx[row_ptr[q]:row_ptr[q + 1]]
+            assert set(range(max(0, q - 49), q + 1)) <= set(row.tolist())
+            assert set(range(0, min(7, q + 1))) <= set(row.tolist())
+            assert np.array_equal(row, geo.row_set(sp, 0, q))
+    sp = spec(density_ppm=1, N=300, window=20, anchor=5)
+    row_ptr, col_idx = geo.build_csr(sp)
+    for q in range(sp.N):
+        row = set(col_idx[row_ptr[q]:row_ptr[q + 1]].tolist())
+        base = set(range(max(0, q - 19), q + 1)) | set(range(0, min(5, q + 1)))
+        assert base <= row and len(row - base) <= 1          # one drawn key at most
+    sp = spec(density_ppm=10**6, N=200, window=16, anchor=3, n_seeds=2)
+    row_ptr, col_idx = geo.build_csr(sp)
+    for q in range(sp.N):
+        assert np.array_equal(col_idx[row_ptr[q]:row_ptr[q + 1]], np.arange(q + 1))
+    sp = spec(density_ppm=30_000, N=900, window=64, anchor=9, n_seeds=4, heads=2)
+    assert geo.nnz_upper_bound(sp) >= geo.build_csr(sp)[0][-1]
