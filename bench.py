@@ -77,7 +77,8 @@ def cpu_baseline(w, layer, Q, K, V, workers, stride):
         # K is rotated once for all rows; charge the sample its share of it.
         t_rope = (time.perf_counter() - t0) * (len(qs) / w.N)
     spec = o_geo.MaskSpec(mode=w.mode, density_ppm=w.density_ppm, seed=w.seed,
-                          n_seeds=w.n_seeds, layer=layer, N=w.N, heads=w.Hkv, block=w.block)
+                          n_seeds=w.n_seeds, layer=layer, N=w.N, heads=w.Hkv, block=w.block,
+                          window=w.window, anchor=w.anchor)
     state = dict(spec=spec, G=w.Hq // w.Hkv, D=w.D, Qr=Qr, Kr=Kr, V=V)
     # Heavy rows (large q) first, interleaved over tasks of 8 rows.
     tasks = [(g, list(qs[::-1][i:i + 8])) for g in range(w.Hkv) for i in range(0, len(qs), 8)]
@@ -109,7 +110,7 @@ def run_gpu(w, layer, Q, K, V, steps, warmup, algo):
     q, k = torch.empty_like(q0), torch.empty_like(k0)
     out = torch.empty(w.Hq, w.N, w.D, dtype=torch.bfloat16, device=dev)
     desc = ris.mask_desc(w.mode, w.density_ppm, w.N, w.Hkv, n_seeds=w.n_seeds, seed=w.seed,
-                         layer=layer, block=w.block)
+                         layer=layer, block=w.block, window=w.window, anchor=w.anchor)
     cap = ris.mask_nnz_bound(desc)
     row_ptr = torch.empty(w.Hkv * w.N + 1, dtype=torch.int64, device=dev)
     col_idx = torch.empty(cap, dtype=torch.int32, device=dev)
@@ -230,6 +231,7 @@ def main():
         "config": {"workload": w.name, "Hq": w.Hq, "Hkv": w.Hkv, "head_dim": w.D, "N": w.N,
                    "mode": "structural" if w.mode == STRUCTURAL else "stochastic",
                    "density": w.density_ppm / 1e6, "seeds": w.n_seeds, "block": w.block,
+                   "window": w.window, "anchor": w.anchor,
                    "rope": ["none", "plain", "linear", "yarn"][w.rope + 1], "layer": args.layer},
         "ms_per_layer_attn": g["ms_attn"],
         "ms_geometry": g["ms_mask"],

@@ -73,6 +73,13 @@ typedef enum { RIS_ATTN_AUTO = 0, RIS_ATTN_GATHER = 1, RIS_ATTN_TILE = 2 } ris_a
  * q) is a keyed Feistel permutation of the pool whose six round keys are the
  * first six 32-bit words of Philox4x64-10(counter = (q, kv_head, layer, 0),
  * key = (s, 0)); a keyed permutation yields distinct keys with no dedupe.
+ *
+ * The full geometry adds two contiguous ranges to the same union (Methods,
+ * "Ensemble Stochastic Projection and Retrieval Coverage": dense local window
+ * plus a global anchor over the initial tokens): the local window
+ * [max(0, q - window + 1), q] and the anchor [0, min(anchor, q + 1)).  They
+ * leave the per-seed draw counts unchanged.  0 disables either; both require
+ * causal = 1.
  */
 typedef struct {
     int32_t  mode;          /* ris_mode                                        */
@@ -85,6 +92,8 @@ typedef struct {
     int32_t  causal;        /* 1 = pool [0, q]; 0 = pool [0, N) (Stochastic)   */
     int32_t  block;         /* Structural block B; 0 = min(N/10, B_max) with   */
                             /* B_max = k evaluated on n = N                    */
+    int32_t  window;        /* local window L (>= 0; 0 = none)                 */
+    int32_t  anchor;        /* initial-token anchor A (>= 0; 0 = none)         */
 } ris_mask_desc;
 
 /*
@@ -113,8 +122,10 @@ int ris_mask_build(const ris_mask_desc* desc, int64_t* row_ptr, int32_t* col_idx
 
 /*
  * Host-only closed-form upper bound on nnz for the descriptor:
- * sum over rows of min(pool, n_seeds * draws) (+ clique), times heads.
- * Exact when n_seeds == 1.  Returns a negative ris_status on a bad descriptor.
+ * sum over rows of min(pool, n_seeds * draws) (+ clique), times heads; with a
+ * window or anchor, each row adds min(window, q+1) + min(anchor, q+1) and is
+ * capped at q + 1.  Exact when n_seeds == 1 and there is no window or anchor.
+ * Returns a negative ris_status on a bad descriptor.
  */
 int64_t ris_mask_nnz_bound(const ris_mask_desc* desc);
 
@@ -191,7 +202,8 @@ int ris_sparse_attn(const void* Q, const void* K, const void* V, const int64_t* 
 /* Human-readable name of a ris_status (static string, never NULL). */
 const char* ris_status_string(int status);
 
-/* Library ABI version: (major << 16) | minor. */
+/* Library ABI version: (major << 16) | minor.  2.0 added window and anchor to
+ * ris_mask_desc. */
 int ris_version(void);
 
 #ifdef __cplusplus

@@ -61,13 +61,30 @@ __device__ __forceinline__ void split_draw(uint32_t idx, uint32_t draws, float i
     if (j >= (int)draws) { ++s; j -= (int)draws; }
 }
 
+// Bits [lo, hi) that fall in word w.
+__device__ __forceinline__ uint32_t range_bits(uint32_t w, uint32_t lo, uint32_t hi) {
+    const uint32_t b0 = w * 32u, b1 = b0 + 32u;
+    const uint32_t a = lo > b0 ? lo : b0, e = hi < b1 ? hi : b1;
+    if (a >= e) return 0u;
+    const uint32_t n = e - a;
+    return (n == 32u ? ~0u : ((1u << n) - 1u)) << (a - b0);
+}
+
 // Fill `bits` (W words, already visible to the whole block) with the union of
-// every seed's draws for row (h, q).  Ends with a block barrier.
+// every seed's draws for row (h, q), on top of the local window and the
+// initial-token anchor clipped to the pool (above the pool they lie inside the
+// Structural clique, which is emitted as a range of its own).  Ends with a
+// block barrier.
 __device__ void build_row_bitmap(const MaskParams& p, int64_t q, int h, const RowGeom& g,
                                  uint32_t* rks, uint32_t* bits) {
     const int tid = threadIdx.x;
     const uint32_t W = (g.pool + 31u) >> 5;
-    for (uint32_t w = tid; w < W; w += kThreads) bits[w] = 0u;
+    const uint32_t qe = (uint32_t)q + 1u;
+    const uint32_t a_hi = min((uint32_t)p.anchor, min(qe, g.pool));
+    const uint32_t w_lo = p.window > 0 && (uint32_t)p.window < qe ? qe - (uint32_t)p.window : 0u;
+    const uint32_t w_hi = p.window > 0 ? min(qe, g.pool) : 0u;
+    for (uint32_t w = tid; w < W; w += kThreads)
+        bits[w] = range_bits(w, 0u, a_hi) | range_bits(w, w_lo, w_hi);
     if (g.draws == 0) {
         __syncthreads();
         return;

@@ -21,7 +21,9 @@ int validate_mask(const ris_mask_desc* d) {
     if (d->heads < 1 || d->heads > 8192) return RIS_E_ARG;
     if (d->causal != 0 && d->causal != 1) return RIS_E_ARG;
     if (d->block < 0) return RIS_E_ARG;
+    if (d->window < 0 || d->anchor < 0) return RIS_E_ARG;
     if (d->mode == RIS_STRUCTURAL && !d->causal) return RIS_E_UNSUPPORTED;
+    if ((d->window > 0 || d->anchor > 0) && !d->causal) return RIS_E_UNSUPPORTED;
     return RIS_OK;
 }
 
@@ -46,16 +48,19 @@ MaskParams make_params(const ris_mask_desc* d) {
     p.heads = d->heads;
     p.causal = d->causal;
     p.block = resolve_block(d);
+    p.window = d->window;
+    p.anchor = d->anchor;
     return p;
 }
 
 int64_t nnz_bound(const MaskParams& p) {
     int64_t total = 0;
     for (int64_t q = 0; q < p.N; ++q) {
+        int64_t row;
         if (p.mode == RIS_STOCHASTIC) {
             const int64_t n = p.causal ? q + 1 : p.N;
             const int64_t k = ris::row_count(p.ppm, n) * p.n_seeds;
-            total += k < n ? k : n;
+            row = k < n ? k : n;
         } else {
             const int64_t start = (q / p.block) * (int64_t)p.block;
             const int64_t clique = q - start + 1;
@@ -63,8 +68,13 @@ int64_t nnz_bound(const MaskParams& p) {
             if (kg < 0) kg = 0;
             if (kg > start) kg = start;
             const int64_t g = kg * p.n_seeds;
-            total += clique + (g < start ? g : start);
+            row = clique + (g < start ? g : start);
         }
+        if (p.window > 0 || p.anchor > 0) {
+            row += (p.window < q + 1 ? p.window : q + 1) + (p.anchor < q + 1 ? p.anchor : q + 1);
+            if (row > q + 1) row = q + 1;
+        }
+        total += row;
     }
     return total * p.heads;
 }
@@ -77,7 +87,7 @@ constexpr float kAutoDensity = 0.06f;
 
 extern "C" {
 
-int ris_version(void) { return (1 << 16) | 0; }
+int ris_version(void) { return (2 << 16) | 0; }
 
 const char* ris_status_string(int status) {
     switch (status) {

@@ -17,6 +17,8 @@ struct MaskParams {
     int32_t heads;
     int32_t causal;
     int32_t block;
+    int32_t window;   // local window L (0 = none)
+    int32_t anchor;   // initial-token anchor A (0 = none)
 };
 
 hipError_t launch_mask_count(const MaskParams& p, int64_t* row_ptr, hipStream_t st);

@@ -28,7 +28,8 @@ class MaskDesc(ctypes.Structure):
     _fields_ = [("mode", ctypes.c_int32), ("density_ppm", ctypes.c_int32),
                 ("seed", ctypes.c_uint64), ("n_seeds", ctypes.c_int32),
                 ("layer", ctypes.c_int32), ("N", ctypes.c_int64), ("heads", ctypes.c_int32),
-                ("causal", ctypes.c_int32), ("block", ctypes.c_int32)]
+                ("causal", ctypes.c_int32), ("block", ctypes.c_int32),
+                ("window", ctypes.c_int32), ("anchor", ctypes.c_int32)]
 
 
 class RopeDesc(ctypes.Structure):
@@ -114,8 +115,10 @@ def _need_device(*ts):
             raise ValueError("tensors must be contiguous GPU tensors")
 
 
-def mask_desc(mode, density_ppm, N, heads, n_seeds=1, seed=0, layer=0, causal=1, block=0):
-    return MaskDesc(mode, density_ppm, seed, n_seeds, layer, N, heads, causal, block)
+def mask_desc(mode, density_ppm, N, heads, n_seeds=1, seed=0, layer=0, causal=1, block=0,
+              window=0, anchor=0):
+    return MaskDesc(mode, density_ppm, seed, n_seeds, layer, N, heads, causal, block, window,
+                    anchor)
 
 
 def mask_nnz_bound(desc):

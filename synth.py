@@ -39,6 +39,8 @@ class Workload:
     layers: int = 1
     needles: bool = False
     seed: int = 0              # first ensemble seed
+    window: int = 0            # dense local window L (0 = none)
+    anchor: int = 0            # initial-token anchor A (0 = none)
 
     def scaled(self, N):
         return replace(self, N=N)
@@ -61,6 +63,12 @@ WORKLOADS = {
     "tinyllama_64k_structural": Workload(
         "tinyllama_64k_structural", 32, 4, 64, 65536, "bf16", STRUCTURAL, 50_000, 10,
         block=64, layers=22),
+    # The 64k Qwen2 layer with the paper's full geometry: the 70-seed ensemble
+    # plus a dense local window of 1,024 tokens and an anchor of 4 initial
+    # tokens (the paper gives no anchor size).
+    "qwen2_64k_full_geometry": Workload(
+        "qwen2_64k_full_geometry", 12, 2, 128, 65536, "bf16", STOCHASTIC, 10_000, 70,
+        rope=ROPE_YARN, rope_base=1e6, rope_orig=32768, window=1024, anchor=4),
 }
 
 

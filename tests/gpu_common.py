@@ -19,14 +19,15 @@ def say(msg):
     print(msg, flush=True)
 
 
-def spec_of(mode, ppm, N, heads, S=1, seed=0, layer=0, causal=1, block=0):
+def spec_of(mode, ppm, N, heads, S=1, seed=0, layer=0, causal=1, block=0, window=0, anchor=0):
     return o_geo.MaskSpec(mode=mode, density_ppm=ppm, seed=seed, n_seeds=S, layer=layer, N=N,
-                          heads=heads, causal=causal, block=block)
+                          heads=heads, causal=causal, block=block, window=window, anchor=anchor)
 
 
 def desc_of(ris, spec):
     return ris.mask_desc(spec.mode, spec.density_ppm, spec.N, spec.heads, n_seeds=spec.n_seeds,
-                         seed=spec.seed, layer=spec.layer, causal=spec.causal, block=spec.block)
+                         seed=spec.seed, layer=spec.layer, causal=spec.causal, block=spec.block,
+                         window=spec.window, anchor=spec.anchor)
 
 
 def gpu_csr(ris, spec, use_bound=False):

@@ -50,12 +50,12 @@ def test_status_strings_and_version(ris):
     for code in (0, -1, -2, -3, -4, -5, -6):
         assert ris.status_string(code).startswith("RIS_")
     assert ris.status_string(123) == "unknown ris_status"
-    assert ris.version() >> 16 == 1
+    assert ris.version() >> 16 == 2
 
 
 def _mask(ris, **kw):
     d = dict(mode=0, density_ppm=10_000, N=512, heads=1, n_seeds=1, seed=0, layer=0,
-             causal=1, block=0)
+             causal=1, block=0, window=0, anchor=0)
     d.update(kw)
     return ris.mask_desc(**d)
 
@@ -64,7 +64,8 @@ def _mask(ris, **kw):
     (dict(density_ppm=0), -1), (dict(density_ppm=1_000_001), -1), (dict(n_seeds=0), -1),
     (dict(n_seeds=4097), -1), (dict(N=0), -1), (dict(N=262145), -1), (dict(heads=0), -1),
     (dict(layer=-1), -1), (dict(mode=2), -1), (dict(causal=2), -1), (dict(block=-1), -1),
-    (dict(mode=1, causal=0), -5),
+    (dict(mode=1, causal=0), -5), (dict(window=-1), -1), (dict(anchor=-3), -1),
+    (dict(causal=0, window=16), -5), (dict(causal=0, anchor=4), -5),
 ])
 def test_mask_validation(ris, bad, code):
     d = _mask(ris, **bad)
@@ -83,16 +84,19 @@ def test_mask_null_pointers(ris):
                             -5, None) == -1
 
 
-@pytest.mark.parametrize("mode,ppm,S,N,heads,block,causal", [
-    (0, 100_000, 1, 512, 1, 0, 1), (0, 10_000, 10, 4096, 2, 0, 1), (0, 10_000, 70, 3000, 2, 0, 1),
-    (1, 10_000, 10, 4096, 2, 64, 1), (1, 50_000, 10, 2000, 4, 64, 1), (1, 10_000, 3, 5000, 1, 0, 1),
-    (0, 250_000, 4, 777, 3, 0, 0), (1, 10**6, 2, 300, 1, 7, 1),
+@pytest.mark.parametrize("mode,ppm,S,N,heads,block,causal,window,anchor", [
+    (0, 100_000, 1, 512, 1, 0, 1, 0, 0), (0, 10_000, 10, 4096, 2, 0, 1, 0, 0),
+    (0, 10_000, 70, 3000, 2, 0, 1, 0, 0), (1, 10_000, 10, 4096, 2, 64, 1, 0, 0),
+    (1, 50_000, 10, 2000, 4, 64, 1, 0, 0), (1, 10_000, 3, 5000, 1, 0, 1, 0, 0),
+    (0, 250_000, 4, 777, 3, 0, 0, 0, 0), (1, 10**6, 2, 300, 1, 7, 1, 0, 0),
+    (0, 10_000, 10, 4096, 2, 0, 1, 1024, 4), (1, 10_000, 10, 4096, 2, 64, 1, 1024, 4),
+    (0, 30_000, 4, 700, 1, 0, 1, 5000, 800), (1, 50_000, 3, 3000, 2, 64, 1, 33, 100),
 ])
-def test_nnz_bound_matches_oracle(ris, mode, ppm, S, N, heads, block, causal):
+def test_nnz_bound_matches_oracle(ris, mode, ppm, S, N, heads, block, causal, window, anchor):
     d = _mask(ris, mode=mode, density_ppm=ppm, n_seeds=S, N=N, heads=heads, block=block,
-              causal=causal)
+              causal=causal, window=window, anchor=anchor)
     spec = o_geo.MaskSpec(mode=mode, density_ppm=ppm, seed=0, n_seeds=S, layer=0, N=N,
-                          heads=heads, causal=causal, block=block)
+                          heads=heads, causal=causal, block=block, window=window, anchor=anchor)
     assert ris.mask_nnz_bound(d) == o_geo.nnz_upper_bound(spec)
 
 

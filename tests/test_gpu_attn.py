@@ -22,7 +22,7 @@ pytestmark = pytest.mark.gpu
 
 
 def run_case(Hq, Hkv, N, D, mode, ppm, S, block=0, dtype_in="bf16", dtype_out="f32",
-             causal=1, seed=0, needles=False, algo=0):
+             causal=1, seed=0, needles=False, algo=0, window=0, anchor=0):
     ris = need_gpu()
     Q, K, V = gaussian_qkv(Hq, Hkv, N, D, seed=seed)
     if needles:
@@ -32,7 +32,7 @@ def run_case(Hq, Hkv, N, D, mode, ppm, S, block=0, dtype_in="bf16", dtype_out="f
         Q, K, V = Qt.float().numpy(), Kt.float().numpy(), Vt.float().numpy()
     else:
         Qt, Kt, Vt = (torch.from_numpy(a) for a in (Q, K, V))
-    sp = spec_of(mode, ppm, N, Hkv, S, 0, 0, causal, block)
+    sp = spec_of(mode, ppm, N, Hkv, S, 0, 0, causal, block, window, anchor)
     rp, ci = gpu_csr(ris, sp)
     qd, kd, vd = Qt.cuda(), Kt.cuda(), Vt.cuda()
     out = torch.empty(Hq, N, D, dtype=torch.float32 if dtype_out == "f32" else torch.bfloat16,
@@ -64,6 +64,10 @@ CASES = [
     (12, 2, 400, 128, 0, 10**6, 1, 0, "bf16", "f32"),         # 100%: dense causal
     (4, 2, 333, 128, 0, 150_000, 2, 0, "bf16", "f32"),        # G = 2
     (12, 2, 600, 128, 0, 400_000, 7, 0, "bf16", "f32", 0),    # non-causal
+    # full geometry: local window and initial-token anchor in the same softmax
+    (12, 2, 3000, 128, 0, 10_000, 10, 0, "bf16", "f32", 1, 1024, 4),
+    (32, 4, 2100, 64, 1, 50_000, 10, 64, "bf16", "bf16", 1, 256, 16),
+    (8, 1, 700, 64, 0, 5_000, 3, 0, "f32", "f32", 1, 100, 7),
 ]
 
 
@@ -72,12 +76,14 @@ CASES = [
 def test_attention_matches_oracle(case, algo):
     Hq, Hkv, N, D, mode, ppm, S, block, din, dout = case[:10]
     causal = case[10] if len(case) > 10 else 1
+    window, anchor = case[11:13] if len(case) > 11 else (0, 0)
     if din == "f32" and algo == 2:
         pytest.skip("the tiled MFMA kernel takes bf16 operands")
     if din == "f32" and algo == 0:
         algo = 1                     # AUTO takes the gather kernel for float32
     say(f"attention parity {case} algo {algo}")
-    got, want, _ = run_case(Hq, Hkv, N, D, mode, ppm, S, block, din, dout, causal, algo=algo)
+    got, want, _ = run_case(Hq, Hkv, N, D, mode, ppm, S, block, din, dout, causal, algo=algo,
+                            window=window, anchor=anchor)
     err = float(np.abs(got - want).max())
     say(f"  max err {err:.3e}")
     if din == "f32":

@@ -8,7 +8,7 @@ from oracle import geometry as o_geo
 pytestmark = pytest.mark.gpu
 
 SMALL = [
-    # mode, ppm, N, heads, S, seed, layer, causal, block
+    # mode, ppm, N, heads, S, seed, layer, causal, block[, window, anchor]
     (0, 100_000, 512, 1, 1, 0, 0, 1, 0),           # the tiny workload
     (0, 10_000, 4097, 2, 10, 0, 0, 1, 0),          # ragged N, 10 seeds
     (1, 10_000, 4097, 2, 10, 0, 0, 1, 64),         # Structural, B = 64
@@ -23,6 +23,14 @@ SMALL = [
     (0, 1, 1000, 1, 300, 9, 2, 1, 0),              # k = 1 rows, 300 seeds (batches of 64)
     (0, 500_000, 1, 1, 4, 0, 0, 1, 0),             # N = 1
     (0, 500_000, 2, 1, 4, 0, 0, 1, 0),             # N = 2
+    # full geometry: + window, anchor
+    (0, 10_000, 4097, 2, 10, 0, 0, 1, 0, 1024, 4),      # L = 1024 with 4 sink tokens
+    (1, 10_000, 4097, 2, 10, 0, 0, 1, 64, 1024, 4),     # window spans many blocks
+    (1, 50_000, 3000, 2, 3, 0, 1, 1, 64, 33, 100),      # window inside / across a block
+    (0, 1, 1500, 1, 2, 0, 0, 1, 0, 1, 1),               # window and anchor of one key
+    (0, 30_000, 700, 1, 4, 0, 0, 1, 0, 5000, 0),        # window wider than N
+    (0, 30_000, 700, 1, 4, 0, 0, 1, 0, 0, 800),         # anchor wider than N
+    (0, 10**6, 300, 1, 2, 0, 0, 1, 0, 17, 3),           # 100% with ranges: the triangle
 ]
 
 
@@ -32,8 +40,7 @@ def test_mask_bit_exact_small(cfg, fused):
     """Both build paths: count + scan + fill (col_idx sized exactly) and the
     one-pass build (col_idx sized from the closed-form bound)."""
     ris = need_gpu()
-    mode, ppm, N, heads, S, seed, layer, causal, block = cfg
-    sp = spec_of(mode, ppm, N, heads, S, seed, layer, causal, block)
+    sp = spec_of(*cfg)
     say(f"mask parity {cfg} fused={fused}")
     rp, ci = gpu_csr(ris, sp, use_bound=fused)
     want_rp, want_ci = o_geo.build_csr(sp)
@@ -73,7 +80,8 @@ def test_mask_capacity_error_writes_nothing():
 
 
 @pytest.mark.parametrize("name", ["qwen2_32k_stochastic", "qwen2_32k_structural",
-                                  "qwen2_64k_stochastic_yarn", "tinyllama_64k_structural"])
+                                  "qwen2_64k_stochastic_yarn", "tinyllama_64k_structural",
+                                  "qwen2_64k_full_geometry"])
 def test_mask_full_size(name):
     """Full-size geometry of each workload: every row's size within its
     closed-form bounds, nnz consistent, sampled rows bit-exact."""
@@ -82,7 +90,8 @@ def test_mask_full_size(name):
     ris = need_gpu()
     w = WORKLOADS[name]
     layer = 21 if w.layers > 1 else 0
-    sp = spec_of(w.mode, w.density_ppm, w.N, w.Hkv, w.n_seeds, w.seed, layer, 1, w.block)
+    sp = spec_of(w.mode, w.density_ppm, w.N, w.Hkv, w.n_seeds, w.seed, layer, 1, w.block,
+                 w.window, w.anchor)
     say(f"full-size mask {name} layer {layer}")
     rp_d, ci_d = gpu_csr(ris, sp, use_bound=True)
     rp = rp_d.cpu().numpy()
@@ -92,6 +101,10 @@ def test_mask_full_size(name):
     lo, hi = kk.copy(), np.minimum(n, w.n_seeds * kk)
     if w.mode == o_geo.STRUCTURAL:
         lo, hi = lo + (q - start + 1), hi + (q - start + 1)
+    if w.window or w.anchor:
+        win, anc = np.minimum(w.window, q + 1), np.minimum(w.anchor, q + 1)
+        lo = np.maximum(lo, np.maximum(win, anc))
+        hi = np.minimum(hi + win + anc, q + 1)
     assert rp[0] == 0 and np.all(counts >= lo) and np.all(counts <= hi)
     rows = sample_rows(w.N, w.Hkv, k_each=10)
     got = rows_of(rp, ci_d, [h * w.N + qq for h, qq in rows])

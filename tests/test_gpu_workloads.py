@@ -22,7 +22,8 @@ def gpu_pipeline(ris, w, Qb, Kb, Vb, layer):
     if w.needles:
         Qn = plant_needles(qd.float().cpu().numpy(), kd.float().cpu().numpy(), needle_plan(w.N))
         qd = to_bf16(Qn.astype(np.float32)).cuda()
-    sp = spec_of(w.mode, w.density_ppm, w.N, w.Hkv, w.n_seeds, w.seed, layer, 1, w.block)
+    sp = spec_of(w.mode, w.density_ppm, w.N, w.Hkv, w.n_seeds, w.seed, layer, 1, w.block,
+                 w.window, w.anchor)
     rp, ci = ris.build_csr(desc_of(ris, sp), "cuda", use_bound=True)
     out = torch.empty(w.Hq, w.N, w.D, dtype=torch.bfloat16, device="cuda")
     ris.sparse_attn(qd, kd, vd, rp, ci, out,
@@ -32,7 +33,8 @@ def gpu_pipeline(ris, w, Qb, Kb, Vb, layer):
 
 
 @pytest.mark.parametrize("name", ["qwen2_32k_stochastic", "qwen2_32k_structural",
-                                  "qwen2_64k_stochastic_yarn", "tinyllama_64k_structural"])
+                                  "qwen2_64k_stochastic_yarn", "tinyllama_64k_structural",
+                                  "qwen2_64k_full_geometry"])
 def test_workload_end_to_end(name):
     ris = need_gpu()
     w = WORKLOADS[name]
