@@ -1,6 +1,8 @@
 """Benchmark of the RIS sparse-attention hot path on one MI355X.
 
-One step = one layer of the hot path over resident synthetic inputs:
+One step = one layer (or, with --all-layers, every layer of the workload back
+to back, each with its own geometry) of the hot path over resident synthetic
+inputs:
 restore Q and K from pristine copies (RoPE rotates in place), RoPE on Q and K,
 geometry (the CSR of the seed-ensemble union, built in one pass into a
 col_idx sized from the closed-form bound), sparse attention.  The
@@ -97,7 +99,7 @@ def cpu_baseline(w, layer, Q, K, V, workers, stride):
 # ---------------------------------------------------------------------------
 # GPU
 # ---------------------------------------------------------------------------
-def run_gpu(w, layer, Q, K, V, steps, warmup, algo):
+def run_gpu(w, layers, Q, K, V, steps, warmup, algo):
     import torch
     from paper_2607_21927_amd import ris
     from synth import to_bf16
@@ -109,56 +111,68 @@ def run_gpu(w, layer, Q, K, V, steps, warmup, algo):
         raise SystemExit("needle workload: run its parity test instead")
     q, k = torch.empty_like(q0), torch.empty_like(k0)
     out = torch.empty(w.Hq, w.N, w.D, dtype=torch.bfloat16, device=dev)
-    desc = ris.mask_desc(w.mode, w.density_ppm, w.N, w.Hkv, n_seeds=w.n_seeds, seed=w.seed,
-                         layer=layer, block=w.block, window=w.window, anchor=w.anchor)
-    cap = ris.mask_nnz_bound(desc)
+    descs = [ris.mask_desc(w.mode, w.density_ppm, w.N, w.Hkv, n_seeds=w.n_seeds, seed=w.seed,
+                           layer=layer, block=w.block, window=w.window, anchor=w.anchor)
+             for layer in layers]
+    # The bound does not depend on the layer index: one buffer serves every layer.
+    cap = ris.mask_nnz_bound(descs[0])
     row_ptr = torch.empty(w.Hkv * w.N + 1, dtype=torch.int64, device=dev)
     col_idx = torch.empty(cap, dtype=torch.int32, device=dev)
     rd = (ris.rope_desc(w.rope, w.rope_base, orig_max_pos=w.rope_orig, factor=w.rope_factor)
           if w.rope != ROPE_NONE else None)
     ad = ris.attn_desc(q, k, out, mode=w.mode, block=w.block, algo=algo)
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(5)]
+    nnz = [0] * len(descs)
 
-    def step(record):
-        q.copy_(q0)
-        k.copy_(k0)
-        if record:
-            ev[0].record()
-        if rd is not None:
-            ris.rope(q, rd)
-            ris.rope(k, rd)
-        if record:
-            ev[1].record()
-        # col_idx sized from the closed-form bound: one call builds the CSR.
-        ris.mask_build(desc, row_ptr, col_idx, col_capacity=cap)
-        if record:
-            ev[2].record()
-        ris.sparse_attn(q, k, v, row_ptr, col_idx, out, ad)
-        if record:
-            ev[3].record()
+    def step(stamps):
+        # One layer after another; with several layers each has its own
+        # geometry (the layer index enters the hash) over the same inputs.
+        for i, desc in enumerate(descs):
+            ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)] if stamps is not None else None
+            q.copy_(q0)
+            k.copy_(k0)
+            if ev:
+                ev[0].record()
+            if rd is not None:
+                ris.rope(q, rd)
+                ris.rope(k, rd)
+            if ev:
+                ev[1].record()
+            # col_idx sized from the closed-form bound: one call builds the CSR.
+            ris.mask_build(desc, row_ptr, col_idx, col_capacity=cap)
+            if ev:
+                ev[2].record()
+            ris.sparse_attn(q, k, v, row_ptr, col_idx, out, ad)
+            if ev:
+                ev[3].record()
+                stamps.append(ev)
+            if stamps is None and len(descs) > 1:
+                nnz[i] = int(row_ptr[-1].item())
 
     for _ in range(warmup):
-        step(False)
+        step(None)
     torch.cuda.synchronize()
+    if len(descs) == 1 or warmup == 0:
+        nnz = None
     t_rope = t_mask = t_attn = 0.0
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    stamps = []
     start.record()
-    per_step = []
     for _ in range(steps):
-        step(True)
-        per_step.append(tuple(ev[:4]))
-        # Fresh events for the next step so every step's stamps survive.
-        ev[:4] = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+        step(stamps)
     end.record()
     torch.cuda.synchronize()
     total_ms = start.elapsed_time(end)
-    for e0, e1, e2, e3 in per_step:
+    for e0, e1, e2, e3 in stamps:
         t_rope += e0.elapsed_time(e1)
         t_mask += e1.elapsed_time(e2)
         t_attn += e2.elapsed_time(e3)
-    nnz = int(row_ptr[-1].item())
+    if nnz is None:
+        if len(descs) == 1:
+            nnz = [int(row_ptr[-1].item())]
+        else:
+            raise SystemExit("several layers need at least one warm-up step (it records nnz)")
     return dict(ms_step=total_ms / steps, ms_rope=t_rope / steps, ms_mask=t_mask / steps,
-                ms_attn=t_attn / steps, nnz=nnz)
+                ms_attn=t_attn / steps, nnz=sum(nnz), layers=len(descs))
 
 
 def measured_traffic(workload, kernel_source):
@@ -186,6 +200,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="qwen2_64k_stochastic_yarn", choices=sorted(WORKLOADS))
     ap.add_argument("--layer", type=int, default=0)
+    ap.add_argument("--all-layers", action="store_true",
+                    help="one step = every layer of the workload back to back (layer 0..L-1)")
     ap.add_argument("--algo", type=int, default=0, help="0 auto, 1 gather, 2 tile")
     ap.add_argument("--cpu-workers", type=int, default=16)
     ap.add_argument("--cpu-stride", type=int, default=64)
@@ -207,10 +223,11 @@ def main():
         cpu = cpu_baseline(w, args.layer, Qb, Kb, Vb, workers, args.cpu_stride)
         del Qb, Kb, Vb
 
-    g = run_gpu(w, args.layer, Q, K, V, args.steps, args.warmup, args.algo)
+    layers = list(range(w.layers)) if args.all_layers else [args.layer]
+    g = run_gpu(w, layers, Q, K, V, args.steps, args.warmup, args.algo)
     G = w.Hq // w.Hkv
     pairs = g["nnz"] * G
-    causal_pairs = w.Hkv * w.N * (w.N + 1) / 2
+    causal_pairs = w.Hkv * w.N * (w.N + 1) / 2 * len(layers)
     alg_bytes = g["nnz"] * KV_PAIR_BYTES[w.D]
     achieved = alg_bytes / (g["ms_attn"] * 1e-3) / 1e9
     tiled = w.dtype == "bf16" and args.algo != 1
@@ -232,8 +249,10 @@ def main():
                    "mode": "structural" if w.mode == STRUCTURAL else "stochastic",
                    "density": w.density_ppm / 1e6, "seeds": w.n_seeds, "block": w.block,
                    "window": w.window, "anchor": w.anchor,
-                   "rope": ["none", "plain", "linear", "yarn"][w.rope + 1], "layer": args.layer},
-        "ms_per_layer_attn": g["ms_attn"],
+                   "rope": ["none", "plain", "linear", "yarn"][w.rope + 1],
+                   "layers": f"0..{len(layers) - 1}" if len(layers) > 1 else args.layer},
+        "ms_per_layer_attn": g["ms_attn"] / len(layers),
+        "ms_attn": g["ms_attn"],
         "ms_geometry": g["ms_mask"],
         "ms_rope": g["ms_rope"],
         "attn_pairs_per_s": pairs / (g["ms_attn"] * 1e-3),

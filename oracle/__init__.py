@@ -1,4 +1,4 @@
-"""CPU oracle for RIS sparse attention (prefill hot path).
+"""CPU oracle for RIS sparse attention (prefill hot path and decode step).
 
 TEST INFRASTRUCTURE ONLY.  This package is the plain, slow, obviously correct
 definition that the GPU library is checked against.  Only the test suite, the
@@ -20,9 +20,11 @@ Modules, in the order the method runs:
                   "Dynamic RoPE Scaling"; Results, "RoPE Scaling").
 * ``attention``-- one softmax over the unified index set (PFUS, Methods,
                   "Hybrid Anchor and Pre-Fusion Unified Softmax") and PV.
+* ``decode``   -- the Hybrid-Anchor generation step: frozen stochastic anchor
+                  plus sliding local window, merged, one softmax (same passage).
 
 Every floating-point step runs in float64.  Readings of the paper where it is
 silent or ambiguous are listed in the module that takes them.
 """
 
-from . import philox, prp, geometry, rope, attention  # noqa: F401
+from . import philox, prp, geometry, rope, attention, decode  # noqa: F401
