@@ -121,6 +121,24 @@ int ris_mask_build(const ris_mask_desc* desc, int64_t* row_ptr, int32_t* col_idx
                    int64_t col_capacity, void* stream);
 
 /*
+ * The same geometry for the rows [q_begin, q_begin + q_count) of every KV head
+ * only: row r = kv_head * q_count + (q - q_begin), so row_ptr holds
+ * heads*q_count + 1 entries.  Phases, capacity rule and errors as in
+ * ris_mask_build (which is this call with q_begin = 0, q_count = N); the
+ * bound is ris_mask_rows_nnz_bound.  Requires 0 <= q_begin and
+ * q_begin + q_count <= N.  Serves chunked prefill and the decode anchor: the
+ * stochastic anchor of a sequence whose first generated token sits at
+ * position t0 is row t0 (q_begin = t0, q_count = 1) of a descriptor with
+ * window = anchor = 0 (Methods, "Hybrid Anchor and Pre-Fusion Unified
+ * Softmax").
+ */
+int ris_mask_build_rows(const ris_mask_desc* desc, int64_t q_begin, int64_t q_count,
+                        int64_t* row_ptr, int32_t* col_idx, int64_t col_capacity, void* stream);
+
+/* ris_mask_nnz_bound restricted to the rows [q_begin, q_begin + q_count). */
+int64_t ris_mask_rows_nnz_bound(const ris_mask_desc* desc, int64_t q_begin, int64_t q_count);
+
+/*
  * Host-only closed-form upper bound on nnz for the descriptor:
  * sum over rows of min(pool, n_seeds * draws) (+ clique), times heads; with a
  * window or anchor, each row adds min(window, q+1) + min(anchor, q+1) and is
@@ -199,11 +217,65 @@ typedef struct {
 int ris_sparse_attn(const void* Q, const void* K, const void* V, const int64_t* row_ptr,
                     const int32_t* col_idx, void* out, const ris_attn_desc* desc, void* stream);
 
+/* ------------------------------------------------------------------------ */
+/* Decode step with the Hybrid Anchor                                       */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * One generated token per sequence of a batch (Methods, "Hybrid Anchor and
+ * Pre-Fusion Unified Softmax"): the stochastic anchor, computed once at the
+ * first generated position and cached, merges with the local window of the
+ * current position and the initial tokens, every index once, and each query
+ * head takes one softmax over the merged set.
+ */
+typedef struct {
+    int32_t dtype_in;        /* ris_dtype of Q and the K/V caches: RIS_BF16    */
+    int32_t dtype_out;       /* ris_dtype of out                               */
+    int32_t batch;           /* B sequences (B * Hkv <= 65535)                  */
+    int32_t Hq;              /* query heads                                    */
+    int32_t Hkv;             /* KV heads; G = Hq / Hkv <= 8                     */
+    int32_t D;               /* head dimension: 64 or 128                      */
+    int64_t max_len;         /* cache capacity per (sequence, kv head)         */
+    int64_t anchor_stride;   /* anchor entries reserved per sequence           */
+    int32_t window;          /* local window L (>= 0; 0 = none)                */
+    int32_t sink;            /* initial tokens A (>= 0; 0 = none)               */
+    float   scale;           /* score scale; 0 = 1 / sqrt(D)                    */
+} ris_decode_desc;
+
+/* Bytes of device workspace ris_decode_attn needs for the descriptor (host
+ * only; negative ris_status on a bad descriptor). */
+int64_t ris_decode_workspace_bytes(const ris_decode_desc* desc);
+
+/*
+ * out[b, h, :] = sum_{j in I_b,g} softmax_j(scale <Q[b,h], K[b,g,j]>) V[b,g,j],
+ * g = floor(h / G), t = pos[b],
+ * I_b,g = unique({j in anchor row (b, g) : j <= t} U [max(0, t - L + 1), t]
+ *                U [0, min(A, t + 1))).
+ *
+ * Q, out: device [B, Hq, D].  K, V: device [B, Hkv, max_len, D] caches that
+ * already hold the token at position pos[b].  pos: device int64[B].
+ * anchor_ptr: device int64[B * (Hkv + 1)]; sequence b's anchor is a CSR of
+ * Hkv rows with offsets anchor_ptr[b*(Hkv+1) .. b*(Hkv+1)+Hkv] into its slice
+ * anchor_idx[b*anchor_stride .. (b+1)*anchor_stride) -- exactly what
+ * ris_mask_build_rows(desc, t0, 1, ...) writes into those two slices.
+ * workspace: device memory of at least ris_decode_workspace_bytes(desc)
+ * bytes (RIS_E_CAPACITY otherwise); its contents need no initialisation.
+ * Reads stay inside the buffers as described whatever the device data hold:
+ * offsets are clipped to [0, anchor_stride], anchor entries outside
+ * [0, t] are ignored, and a sequence whose pos lies outside [0, max_len)
+ * gets zeros, as does an empty set.  Accumulation is float32; the softmax
+ * weights enter the PV product rounded to bf16.
+ */
+int ris_decode_attn(const void* Q, const void* K, const void* V, const int64_t* pos,
+                    const int64_t* anchor_ptr, const int32_t* anchor_idx, void* out,
+                    void* workspace, int64_t workspace_bytes, const ris_decode_desc* desc,
+                    void* stream);
+
 /* Human-readable name of a ris_status (static string, never NULL). */
 const char* ris_status_string(int status);
 
 /* Library ABI version: (major << 16) | minor.  2.0 added window and anchor to
- * ris_mask_desc. */
+ * ris_mask_desc; 2.1 added the row-range build and the decode step. */
 int ris_version(void);
 
 #ifdef __cplusplus

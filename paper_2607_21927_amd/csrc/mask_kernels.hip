@@ -164,10 +164,13 @@ __device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* r
     return before + inc - v;
 }
 
-__device__ __forceinline__ void row_of_block(const MaskParams& p, int64_t& q, int& h) {
+// Workgroup -> (row r, query q, head h), heavy (late) rows first.
+__device__ __forceinline__ void row_of_block(const MaskParams& p, int64_t& r, int64_t& q, int& h) {
     const int64_t i = blockIdx.x;
-    q = p.N - 1 - i / p.heads;
+    const int64_t local = p.nq - 1 - i / p.heads;
     h = (int)(i % p.heads);
+    q = p.q0 + local;
+    r = (int64_t)h * p.nq + local;
 }
 
 __global__ __launch_bounds__(kThreads) void k_mask_count(MaskParams p, int64_t* row_ptr) {
@@ -175,15 +178,15 @@ __global__ __launch_bounds__(kThreads) void k_mask_count(MaskParams p, int64_t* 
     __shared__ uint32_t red[4];
     uint32_t* rks = smem;
     uint32_t* bits = smem + kSeedBatch * 6;
-    int64_t q; int h;
-    row_of_block(p, q, h);
+    int64_t r, q; int h;
+    row_of_block(p, r, q, h);
     const RowGeom g = row_geometry(p, q);
     build_row_bitmap(p, q, h, g, rks, bits);
     const uint32_t W = (g.pool + 31u) >> 5;
     uint32_t c = 0;
     for (uint32_t w = threadIdx.x; w < W; w += kThreads) c += __popc(bits[w]);
     const uint32_t total = block_sum(c, red);
-    if (threadIdx.x == 0) row_ptr[(int64_t)h * p.N + q + 1] = (int64_t)total + g.clique_len;
+    if (threadIdx.x == 0) row_ptr[r + 1] = (int64_t)total + g.clique_len;
 }
 
 __global__ __launch_bounds__(kThreads) void k_mask_fill(MaskParams p, const int64_t* row_ptr,
@@ -192,9 +195,8 @@ __global__ __launch_bounds__(kThreads) void k_mask_fill(MaskParams p, const int6
     __shared__ uint32_t red[4];
     uint32_t* rks = smem;
     uint32_t* bits = smem + kSeedBatch * 6;
-    int64_t q; int h;
-    row_of_block(p, q, h);
-    const int64_t r = (int64_t)h * p.N + q;
+    int64_t r, q; int h;
+    row_of_block(p, r, q, h);
     const int64_t base = row_ptr[r];
     int64_t limit = row_ptr[r + 1] - base;
     // Never write outside col_idx[0, capacity), whatever row_ptr holds.
@@ -255,7 +257,7 @@ __global__ __launch_bounds__(kThreads) void k_mask_fused(MaskParams p, int64_t* 
     __shared__ int64_t s_ticket, s_base;
     uint32_t* rks = smem;
     uint32_t* bits = smem + kSeedBatch * 6;
-    const int64_t R = (int64_t)p.heads * p.N;
+    const int64_t R = (int64_t)p.heads * p.nq;
     if (threadIdx.x == 0) {
         const int64_t t = (int64_t)atomicAdd(reinterpret_cast<unsigned long long*>(row_ptr), 1ull);
         s_ticket = t;
@@ -264,8 +266,8 @@ __global__ __launch_bounds__(kThreads) void k_mask_fused(MaskParams p, int64_t* 
     }
     __syncthreads();
     const int64_t r = s_ticket;
-    const int h = (int)(r / p.N);
-    const int64_t q = r - (int64_t)h * p.N;
+    const int h = (int)(r / p.nq);
+    const int64_t q = p.q0 + (r - (int64_t)h * p.nq);
     const RowGeom g = row_geometry(p, q);
     build_row_bitmap(p, q, h, g, rks, bits);
     const uint32_t W = (g.pool + 31u) >> 5;
@@ -386,14 +388,16 @@ __global__ __launch_bounds__(kScanThreads) void k_scan_rows(int64_t* row_ptr, in
 }
 
 size_t mask_smem_bytes(const MaskParams& p) {
-    const int64_t words = (p.N + 31) / 32;
+    // Largest pool of the built rows: q0 + nq keys (causal) or N.
+    const int64_t span = p.causal ? p.q0 + p.nq : p.N;
+    const int64_t words = (span + 31) / 32;
     return (size_t)(kSeedBatch * 6 + words) * sizeof(uint32_t);
 }
 
 }  // namespace
 
 hipError_t launch_mask_count(const MaskParams& p, int64_t* row_ptr, hipStream_t st) {
-    const int64_t rows = (int64_t)p.heads * p.N;
+    const int64_t rows = (int64_t)p.heads * p.nq;
     hipLaunchKernelGGL(k_mask_count, dim3((unsigned)rows), dim3(kThreads), mask_smem_bytes(p), st, p,
                        row_ptr);
     hipError_t e = hipGetLastError();
@@ -404,7 +408,7 @@ hipError_t launch_mask_count(const MaskParams& p, int64_t* row_ptr, hipStream_t 
 
 hipError_t launch_mask_fused(const MaskParams& p, int64_t* row_ptr, int32_t* col_idx,
                              int64_t capacity, hipStream_t st) {
-    const int64_t rows = (int64_t)p.heads * p.N;
+    const int64_t rows = (int64_t)p.heads * p.nq;
     const unsigned eb = (unsigned)((rows + 1 + 255) / 256);
     hipLaunchKernelGGL(k_fill_i64, dim3(eb), dim3(256), 0, st, row_ptr, rows + 1, (int64_t)0);
     hipError_t e = hipGetLastError();
@@ -419,7 +423,7 @@ hipError_t launch_mask_fused(const MaskParams& p, int64_t* row_ptr, int32_t* col
 
 hipError_t launch_mask_fill(const MaskParams& p, const int64_t* row_ptr, int32_t* col_idx,
                             int64_t capacity, hipStream_t st) {
-    const int64_t rows = (int64_t)p.heads * p.N;
+    const int64_t rows = (int64_t)p.heads * p.nq;
     hipLaunchKernelGGL(k_mask_fill, dim3((unsigned)rows), dim3(kThreads), mask_smem_bytes(p), st, p,
                        row_ptr, col_idx, capacity);
     return hipGetLastError();

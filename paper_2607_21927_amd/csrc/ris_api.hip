@@ -27,6 +27,15 @@ int validate_mask(const ris_mask_desc* d) {
     return RIS_OK;
 }
 
+// Rows [q_begin, q_begin + q_count) of every head; one workgroup per row.
+int validate_rows(const ris_mask_desc* d, int64_t q_begin, int64_t q_count) {
+    const int st = validate_mask(d);
+    if (st != RIS_OK) return st;
+    if (q_begin < 0 || q_count < 1 || q_begin > d->N - q_count) return RIS_E_ARG;
+    if ((int64_t)d->heads * q_count > 0x7FFFFFFFll) return RIS_E_UNSUPPORTED;
+    return RIS_OK;
+}
+
 // Structural block size: explicit, or min(floor(N / 10), B_max) with B_max the
 // count rule evaluated on n = N (at least 1).
 int32_t resolve_block(const ris_mask_desc* d) {
@@ -37,8 +46,10 @@ int32_t resolve_block(const ris_mask_desc* d) {
     return b < 1 ? 1 : (int32_t)b;
 }
 
-MaskParams make_params(const ris_mask_desc* d) {
+MaskParams make_params(const ris_mask_desc* d, int64_t q0, int64_t nq) {
     MaskParams p;
+    p.q0 = q0;
+    p.nq = nq;
     p.seed = d->seed;
     p.N = d->N;
     p.mode = d->mode;
@@ -55,7 +66,7 @@ MaskParams make_params(const ris_mask_desc* d) {
 
 int64_t nnz_bound(const MaskParams& p) {
     int64_t total = 0;
-    for (int64_t q = 0; q < p.N; ++q) {
+    for (int64_t q = p.q0; q < p.q0 + p.nq; ++q) {
         int64_t row;
         if (p.mode == RIS_STOCHASTIC) {
             const int64_t n = p.causal ? q + 1 : p.N;
@@ -87,7 +98,7 @@ constexpr float kAutoDensity = 0.06f;
 
 extern "C" {
 
-int ris_version(void) { return (2 << 16) | 0; }
+int ris_version(void) { return (2 << 16) | 1; }
 
 const char* ris_status_string(int status) {
     switch (status) {
@@ -102,18 +113,23 @@ const char* ris_status_string(int status) {
     }
 }
 
-int64_t ris_mask_nnz_bound(const ris_mask_desc* desc) {
-    const int st = validate_mask(desc);
+int64_t ris_mask_rows_nnz_bound(const ris_mask_desc* desc, int64_t q_begin, int64_t q_count) {
+    const int st = validate_rows(desc, q_begin, q_count);
     if (st != RIS_OK) return st;
-    return nnz_bound(make_params(desc));
+    return nnz_bound(make_params(desc, q_begin, q_count));
 }
 
-int ris_mask_build(const ris_mask_desc* desc, int64_t* row_ptr, int32_t* col_idx,
-                   int64_t col_capacity, void* stream) {
-    const int st = validate_mask(desc);
+int64_t ris_mask_nnz_bound(const ris_mask_desc* desc) {
+    if (!desc) return RIS_E_ARG;
+    return ris_mask_rows_nnz_bound(desc, 0, desc->N);
+}
+
+int ris_mask_build_rows(const ris_mask_desc* desc, int64_t q_begin, int64_t q_count,
+                        int64_t* row_ptr, int32_t* col_idx, int64_t col_capacity, void* stream) {
+    const int st = validate_rows(desc, q_begin, q_count);
     if (st != RIS_OK) return st;
     if (!row_ptr) return RIS_E_ARG;
-    const MaskParams p = make_params(desc);
+    const MaskParams p = make_params(desc, q_begin, q_count);
     hipStream_t s = static_cast<hipStream_t>(stream);
     if (!col_idx) return hip_status(ris::launch_mask_count(p, row_ptr, s));
     if (col_capacity < 0) return RIS_E_ARG;
@@ -122,13 +138,19 @@ int ris_mask_build(const ris_mask_desc* desc, int64_t* row_ptr, int32_t* col_idx
         return hip_status(ris::launch_mask_fused(p, row_ptr, col_idx, col_capacity, s));
     {
         int64_t nnz = 0;
-        const int64_t rows = (int64_t)p.heads * p.N;
+        const int64_t rows = (int64_t)p.heads * p.nq;
         if (hipMemcpyAsync(&nnz, row_ptr + rows, sizeof(nnz), hipMemcpyDeviceToHost, s) != hipSuccess)
             return RIS_E_HIP;
         if (hipStreamSynchronize(s) != hipSuccess) return RIS_E_HIP;
         if (nnz > col_capacity || nnz < 0) return RIS_E_CAPACITY;
     }
     return hip_status(ris::launch_mask_fill(p, row_ptr, col_idx, col_capacity, s));
+}
+
+int ris_mask_build(const ris_mask_desc* desc, int64_t* row_ptr, int32_t* col_idx,
+                   int64_t col_capacity, void* stream) {
+    if (!desc) return RIS_E_ARG;
+    return ris_mask_build_rows(desc, 0, desc->N, row_ptr, col_idx, col_capacity, stream);
 }
 
 int ris_rope(void* x, int32_t dtype, int32_t heads, int64_t N, int32_t D, int64_t pos0,
@@ -220,6 +242,81 @@ int ris_sparse_attn(const void* Q, const void* K, const void* V, const int64_t* 
     const int st = hip_status(ris::launch_attn_tile(a, s));
     if (st != RIS_OK) return st;
     return hip_status(ris::launch_attn_gather(a, s));
+}
+
+}  // extern "C"
+
+// ---- decode step
+
+namespace {
+
+int64_t decode_parts(const ris_decode_desc& d) {
+    const int64_t win = d.window < d.max_len ? d.window : d.max_len;
+    const int64_t snk = d.sink < d.max_len ? d.sink : d.max_len;
+    const int64_t keys = d.anchor_stride + win + snk;
+    int64_t chunks = (keys + ris::kDecodeChunkKeys - 1) / ris::kDecodeChunkKeys;
+    if (chunks < 1) chunks = 1;
+    return chunks * ris::kDecodeWaves;
+}
+
+int validate_decode(const ris_decode_desc* d) {
+    if (!d) return RIS_E_ARG;
+    if (d->dtype_in != RIS_F32 && d->dtype_in != RIS_BF16) return RIS_E_DTYPE;
+    if (d->dtype_out != RIS_F32 && d->dtype_out != RIS_BF16) return RIS_E_DTYPE;
+    if (d->dtype_in != RIS_BF16) return RIS_E_UNSUPPORTED;
+    if (d->batch < 1 || d->Hq < 1 || d->Hkv < 1) return RIS_E_ARG;
+    if (d->Hq % d->Hkv != 0) return RIS_E_SHAPE;
+    if (d->Hq / d->Hkv > 8) return RIS_E_UNSUPPORTED;
+    if (d->D != 64 && d->D != 128) return RIS_E_UNSUPPORTED;
+    if (d->max_len < 1 || d->max_len > (1ll << 31)) return RIS_E_ARG;
+    if (d->anchor_stride < 0 || d->anchor_stride > (1ll << 40)) return RIS_E_ARG;
+    if (d->window < 0 || d->sink < 0) return RIS_E_ARG;
+    if (!(d->scale >= 0.0f) || !isfinite(d->scale)) return RIS_E_ARG;
+    if ((int64_t)d->batch * d->Hkv > 65535) return RIS_E_UNSUPPORTED;
+    if ((int64_t)d->batch * d->Hq > 0x7FFFFFFFll) return RIS_E_UNSUPPORTED;
+    if (decode_parts(*d) > (1ll << 30)) return RIS_E_UNSUPPORTED;
+    return RIS_OK;
+}
+
+int64_t decode_workspace(const ris_decode_desc& d) {
+    const int64_t per = (int64_t)d.batch * d.Hkv * decode_parts(d) * (d.Hq / d.Hkv);
+    return per * (d.D + 2) * (int64_t)sizeof(float);
+}
+
+}  // namespace
+
+extern "C" {
+
+int64_t ris_decode_workspace_bytes(const ris_decode_desc* desc) {
+    const int st = validate_decode(desc);
+    if (st != RIS_OK) return st;
+    return decode_workspace(*desc);
+}
+
+int ris_decode_attn(const void* Q, const void* K, const void* V, const int64_t* pos,
+                    const int64_t* anchor_ptr, const int32_t* anchor_idx, void* out,
+                    void* workspace, int64_t workspace_bytes, const ris_decode_desc* desc,
+                    void* stream) {
+    const int st = validate_decode(desc);
+    if (st != RIS_OK) return st;
+    if (!Q || !K || !V || !pos || !anchor_ptr || !out || !workspace) return RIS_E_ARG;
+    if (!anchor_idx && desc->anchor_stride > 0) return RIS_E_ARG;
+    if (workspace_bytes < decode_workspace(*desc)) return RIS_E_CAPACITY;
+    const ris_decode_desc& d = *desc;
+    ris::DecodeParams p;
+    p.Q = Q; p.K = K; p.V = V;
+    p.pos = pos; p.anchor_ptr = anchor_ptr; p.anchor_idx = anchor_idx;
+    p.out = out;
+    p.max_len = d.max_len; p.anchor_stride = d.anchor_stride;
+    p.B = d.batch; p.Hq = d.Hq; p.Hkv = d.Hkv; p.G = d.Hq / d.Hkv; p.D = d.D;
+    p.out_bf16 = d.dtype_out == RIS_BF16;
+    p.window = d.window; p.sink = d.sink;
+    p.parts = (int32_t)decode_parts(d);
+    p.scale = d.scale > 0.0f ? d.scale : 1.0f / sqrtf((float)d.D);
+    const int64_t n_o = (int64_t)d.batch * d.Hkv * p.parts * p.G * d.D;
+    p.part_o = static_cast<float*>(workspace);
+    p.part_ml = p.part_o + n_o;
+    return hip_status(ris::launch_decode(p, static_cast<hipStream_t>(stream)));
 }
 
 }  // extern "C"

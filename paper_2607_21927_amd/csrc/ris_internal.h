@@ -19,6 +19,8 @@ struct MaskParams {
     int32_t block;
     int32_t window;   // local window L (0 = none)
     int32_t anchor;   // initial-token anchor A (0 = none)
+    int64_t q0;       // rows [q0, q0 + nq) of each head are built;
+    int64_t nq;       // row r = h * nq + (q - q0)
 };
 
 hipError_t launch_mask_count(const MaskParams& p, int64_t* row_ptr, hipStream_t st);
@@ -65,5 +67,29 @@ __device__ __forceinline__ bool tile_is_dense(const AttnParams& a, int g, int64_
 }
 hipError_t launch_attn_gather(const AttnParams& a, hipStream_t st);
 hipError_t launch_attn_tile(const AttnParams& a, hipStream_t st);
+
+// Decode step (Hybrid Anchor).  A workgroup of kDecodeWaves waves covers
+// kDecodeChunkKeys keys of one row's virtual key list; every wave writes one
+// partial (its max, sum and unnormalised output per head).
+constexpr int kDecodeWaves = 4;
+constexpr int kDecodeChunkKeys = 1024;
+struct DecodeParams {
+    const void* Q;                // [B, Hq, D] bf16
+    const void* K;                // [B, Hkv, max_len, D] bf16
+    const void* V;
+    const int64_t* pos;           // [B]
+    const int64_t* anchor_ptr;    // [B, Hkv + 1]
+    const int32_t* anchor_idx;    // [B, anchor_stride]
+    void* out;                    // [B, Hq, D]
+    float* part_o;                // [B * Hkv, parts, G, D]
+    float* part_ml;               // [B * Hkv, parts, G, 2]
+    int64_t max_len, anchor_stride;
+    int32_t B, Hq, Hkv, G, D;
+    int32_t out_bf16;
+    int32_t window, sink;
+    int32_t parts;                // partials per row (a multiple of kDecodeWaves)
+    float scale;
+};
+hipError_t launch_decode(const DecodeParams& p, hipStream_t st);
 
 }  // namespace ris

@@ -45,6 +45,14 @@ class AttnDesc(ctypes.Structure):
                 ("block", ctypes.c_int32), ("causal", ctypes.c_int32), ("algo", ctypes.c_int32)]
 
 
+class DecodeDesc(ctypes.Structure):
+    _fields_ = [("dtype_in", ctypes.c_int32), ("dtype_out", ctypes.c_int32),
+                ("batch", ctypes.c_int32), ("Hq", ctypes.c_int32), ("Hkv", ctypes.c_int32),
+                ("D", ctypes.c_int32), ("max_len", ctypes.c_int64),
+                ("anchor_stride", ctypes.c_int64), ("window", ctypes.c_int32),
+                ("sink", ctypes.c_int32), ("scale", ctypes.c_float)]
+
+
 _lib = None
 
 
@@ -60,6 +68,15 @@ def lib():
         L.ris_mask_build.restype = ctypes.c_int
         L.ris_mask_nnz_bound.argtypes = [ctypes.POINTER(MaskDesc)]
         L.ris_mask_nnz_bound.restype = i64
+        L.ris_mask_build_rows.argtypes = [ctypes.POINTER(MaskDesc), i64, i64, vp, vp, i64, vp]
+        L.ris_mask_build_rows.restype = ctypes.c_int
+        L.ris_mask_rows_nnz_bound.argtypes = [ctypes.POINTER(MaskDesc), i64, i64]
+        L.ris_mask_rows_nnz_bound.restype = i64
+        L.ris_decode_workspace_bytes.argtypes = [ctypes.POINTER(DecodeDesc)]
+        L.ris_decode_workspace_bytes.restype = i64
+        L.ris_decode_attn.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, i64,
+                                      ctypes.POINTER(DecodeDesc), vp]
+        L.ris_decode_attn.restype = ctypes.c_int
         L.ris_rope.argtypes = [vp, i32, i32, i64, i32, i64, ctypes.POINTER(RopeDesc), vp]
         L.ris_rope.restype = ctypes.c_int
         L.ris_sparse_attn.argtypes = [vp, vp, vp, vp, vp, vp, ctypes.POINTER(AttnDesc), vp]
@@ -72,8 +89,9 @@ def lib():
     return _lib
 
 
-EXPORTS = ("ris_mask_build", "ris_mask_nnz_bound", "ris_rope", "ris_sparse_attn",
-           "ris_status_string", "ris_version")
+EXPORTS = ("ris_mask_build", "ris_mask_nnz_bound", "ris_mask_build_rows",
+           "ris_mask_rows_nnz_bound", "ris_rope", "ris_sparse_attn",
+           "ris_decode_workspace_bytes", "ris_decode_attn", "ris_status_string", "ris_version")
 
 
 def status_string(status):
@@ -139,6 +157,67 @@ def mask_build(desc, row_ptr, col_idx=None, col_capacity=None, stream=None):
     cap = col_idx.numel() if (col_idx is not None and col_capacity is None) else (col_capacity or 0)
     _check(lib().ris_mask_build(ctypes.byref(desc), _ptr(row_ptr), _ptr(col_idx), cap,
                                 _stream(stream)), "ris_mask_build")
+
+
+def mask_rows_nnz_bound(desc, q_begin, q_count):
+    v = lib().ris_mask_rows_nnz_bound(ctypes.byref(desc), q_begin, q_count)
+    if v < 0:
+        raise RisError(int(v), "ris_mask_rows_nnz_bound")
+    return int(v)
+
+
+def mask_build_rows(desc, q_begin, q_count, row_ptr, col_idx=None, col_capacity=None,
+                    stream=None):
+    """ris_mask_build_rows: rows [q_begin, q_begin + q_count) of every head.
+    row_ptr and col_idx may be views into larger buffers (e.g. one sequence's
+    slice of a batched anchor cache)."""
+    import torch
+    if row_ptr.dtype != torch.int64 or row_ptr.numel() != desc.heads * q_count + 1:
+        raise ValueError("row_ptr must be int64[heads*q_count + 1]")
+    if not row_ptr.is_cuda or row_ptr.stride(0) != 1:
+        raise ValueError("row_ptr must be a dense GPU vector")
+    if col_idx is not None and (col_idx.dtype != torch.int32 or not col_idx.is_cuda
+                                or col_idx.stride(0) != 1):
+        raise ValueError("col_idx must be a dense int32 GPU vector")
+    cap = col_idx.numel() if (col_idx is not None and col_capacity is None) else (col_capacity or 0)
+    _check(lib().ris_mask_build_rows(ctypes.byref(desc), q_begin, q_count, _ptr(row_ptr),
+                                     _ptr(col_idx), cap, _stream(stream)), "ris_mask_build_rows")
+
+
+def decode_desc(Q, K, out, anchor_stride, window=0, sink=0, scale=0.0):
+    """Descriptor from Q [B, Hq, D], the cache K [B, Hkv, max_len, D] and out."""
+    B, Hq, D = Q.shape
+    return DecodeDesc(_dtype_code(Q), _dtype_code(out), B, Hq, K.shape[1], D, K.shape[2],
+                      anchor_stride, window, sink, scale)
+
+
+def decode_workspace_bytes(desc):
+    v = lib().ris_decode_workspace_bytes(ctypes.byref(desc))
+    if v < 0:
+        raise RisError(int(v), "ris_decode_workspace_bytes")
+    return int(v)
+
+
+def decode_attn(Q, K, V, pos, anchor_ptr, anchor_idx, out, workspace, desc, stream=None):
+    """ris_decode_attn; workspace is a device uint8 tensor of at least
+    decode_workspace_bytes(desc) bytes."""
+    import torch
+    _need_device(Q, K, V, pos, anchor_ptr, anchor_idx, out, workspace)
+    if pos.dtype != torch.int64 or anchor_ptr.dtype != torch.int64:
+        raise TypeError("pos and anchor_ptr must be int64")
+    if anchor_idx.dtype != torch.int32:
+        raise TypeError("anchor_idx must be int32")
+    if pos.numel() != desc.batch or anchor_ptr.numel() != desc.batch * (desc.Hkv + 1):
+        raise ValueError("pos must hold B entries and anchor_ptr B * (Hkv + 1)")
+    if anchor_idx.numel() < desc.batch * desc.anchor_stride:
+        raise ValueError("anchor_idx must hold B * anchor_stride entries")
+    if not (Q.dtype == K.dtype == V.dtype) or K.shape != V.shape:
+        raise TypeError("Q, K, V must share a dtype and K, V a shape")
+    nbytes = workspace.numel() * workspace.element_size()
+    _check(lib().ris_decode_attn(_ptr(Q), _ptr(K), _ptr(V), _ptr(pos), _ptr(anchor_ptr),
+                                 _ptr(anchor_idx), _ptr(out), _ptr(workspace), nbytes,
+                                 ctypes.byref(desc), _stream(stream)), "ris_decode_attn")
+    return out
 
 
 def rope(x, desc, pos0=0, stream=None):

@@ -132,3 +132,14 @@ def plant_needles(Q, K, plan, sigma_mult=3.0):
         for h in range(g * G, (g + 1) * G):
             np.add.at(Q[h], i, add)
     return Q
+
+
+def decode_inputs(B, Hq, Hkv, max_len, D, seed=0):
+    """Decode-step inputs ~ N(0,1) float32, drawn in this order from
+    ``numpy.random.default_rng(seed)``: the new tokens' queries Q [B, Hq, D]
+    and the caches K, V [B, Hkv, max_len, D]."""
+    rng = np.random.default_rng(seed)
+    Q = rng.standard_normal((B, Hq, D), dtype=np.float32)
+    K = rng.standard_normal((B, Hkv, max_len, D), dtype=np.float32)
+    V = rng.standard_normal((B, Hkv, max_len, D), dtype=np.float32)
+    return Q, K, V

@@ -32,8 +32,10 @@ def declared_functions():
 
 def test_header_declares_the_boundary():
     names = declared_functions()
-    assert names == sorted(["ris_mask_build", "ris_mask_nnz_bound", "ris_rope",
-                            "ris_sparse_attn", "ris_status_string", "ris_version"])
+    assert names == sorted(["ris_mask_build", "ris_mask_nnz_bound", "ris_mask_build_rows",
+                            "ris_mask_rows_nnz_bound", "ris_rope", "ris_sparse_attn",
+                            "ris_decode_workspace_bytes", "ris_decode_attn",
+                            "ris_status_string", "ris_version"])
 
 
 def test_library_exports_every_declared_symbol(ris):
@@ -141,3 +143,52 @@ def test_attn_validation(ris):
     d = ris.AttnDesc(1, 0, 12, 2, 64, 128, 0.0, 0, 0, 1, 0)
     assert L.ris_sparse_attn(None, p, p, p, p, p, ctypes.byref(d), None) == -1
     assert L.ris_sparse_attn(p, p, p, p, p, None, ctypes.byref(d), None) == -1
+
+
+def test_mask_rows_validation_and_bound(ris):
+    L = ris.lib()
+    d = _mask(ris, N=1000, n_seeds=3)
+    fake = ctypes.c_void_p(0x1000)
+    for q0, nq in [(-1, 5), (0, 0), (999, 2), (1000, 1), (0, 1001)]:
+        assert L.ris_mask_rows_nnz_bound(ctypes.byref(d), q0, nq) == -1
+        assert L.ris_mask_build_rows(ctypes.byref(d), q0, nq, fake, None, 0, None) == -1
+    assert ris.mask_rows_nnz_bound(d, 0, 1000) == ris.mask_nnz_bound(d)
+    for dd in [d, _mask(ris, mode=1, N=1000, block=64, window=100, anchor=4, n_seeds=5)]:
+        a = ris.mask_rows_nnz_bound(dd, 100, 300)
+        b = ris.mask_rows_nnz_bound(dd, 400, 250)
+        assert a + b == ris.mask_rows_nnz_bound(dd, 100, 550)
+    huge = _mask(ris, N=262144, heads=8192)
+    assert L.ris_mask_nnz_bound(ctypes.byref(huge)) == -5
+
+
+def _decode(ris, **kw):
+    d = dict(dtype_in=1, dtype_out=0, batch=2, Hq=12, Hkv=2, D=128, max_len=4096,
+             anchor_stride=1000, window=1024, sink=4, scale=0.0)
+    d.update(kw)
+    return ris.DecodeDesc(**d)
+
+
+@pytest.mark.parametrize("bad,code", [
+    (dict(dtype_in=0), -5), (dict(dtype_in=3), -3), (dict(dtype_out=7), -3), (dict(D=96), -5),
+    (dict(Hq=13), -2), (dict(Hq=18), -5), (dict(batch=0), -1), (dict(Hkv=0), -1),
+    (dict(max_len=0), -1), (dict(anchor_stride=-1), -1), (dict(window=-1), -1),
+    (dict(sink=-2), -1), (dict(scale=-1.0), -1), (dict(batch=40000), -5),
+])
+def test_decode_validation(ris, bad, code):
+    d = _decode(ris, **bad)
+    L = ris.lib()
+    assert L.ris_decode_workspace_bytes(ctypes.byref(d)) == code
+    f = ctypes.c_void_p(0x1000)       # never dereferenced: validation fails first
+    assert L.ris_decode_attn(f, f, f, f, f, f, f, f, 1 << 40, ctypes.byref(d), None) == code
+
+
+def test_decode_workspace_size_and_capacity_error(ris):
+    d = _decode(ris)
+    # 2 sequences x 2 kv heads x 8 partials (1000 + 1024 + 4 keys -> 2 chunks
+    # of 1024 keys, 4 waves each) x 6 heads x (128 + 2) floats
+    assert ris.decode_workspace_bytes(d) == 2 * 2 * 8 * 6 * 130 * 4
+    L = ris.lib()
+    f = ctypes.c_void_p(0x1000)
+    need = ris.decode_workspace_bytes(d)
+    assert L.ris_decode_attn(f, f, f, f, f, f, f, f, need - 1, ctypes.byref(d), None) == -4
+    assert L.ris_decode_attn(f, f, f, f, f, None, f, f, need, ctypes.byref(d), None) == -1
