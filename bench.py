@@ -193,6 +193,126 @@ def measured_traffic(workload, kernel_source):
     return float(rec["traffic_bytes"])
 
 
+# ---------------------------------------------------------------------------
+# Decode step (Hybrid Anchor): --decode
+# ---------------------------------------------------------------------------
+def decode_pairs(aptr, aidx, stride, t0s, ts, Hkv, window, sink):
+    """kv-pairs attended by one decode step: per (sequence, kv head) the
+    anchor entries outside the window and the initial range, plus both."""
+    total = 0
+    for b, t in enumerate(ts):
+        w_lo = max(0, t - window + 1) if window > 0 else t + 1
+        s_hi = min(sink, w_lo)
+        for g in range(Hkv):
+            lo, hi = aptr[b * (Hkv + 1) + g], aptr[b * (Hkv + 1) + g + 1]
+            a = aidx[b * stride + lo:b * stride + hi]
+            total += int(((a >= s_hi) & (a < w_lo)).sum()) + (t + 1 - w_lo) + s_hi
+    return total
+
+
+def cpu_decode_baseline(w, t0s, ts, Q, K, V, rows):
+    """The oracle's decode step on a few (sequence, kv head) rows."""
+    from oracle import decode as o_dec
+    from oracle import geometry as o_geo
+    sp = o_geo.MaskSpec(mode=w.mode, density_ppm=w.density_ppm, seed=w.seed,
+                        n_seeds=w.n_seeds, layer=0, N=K.shape[2], heads=w.Hkv, block=w.block)
+    G = w.Hq // w.Hkv
+    t0 = time.perf_counter()
+    pairs = 0
+    for b, g in rows:
+        anc = o_dec.stochastic_anchor(sp, g, t0s[b])
+        idx = o_dec.step_set(anc, ts[b], w.window, w.anchor)
+        o_dec.decode_attention(Q[b, g * G:(g + 1) * G], K[b, g], V[b, g], idx, w.D ** -0.5)
+        pairs += len(idx) * G
+    wall = time.perf_counter() - t0
+    return {"value": pairs / wall, "unit": "pairs/s", "cores": 1, "kind": "oracle",
+            "sample": f"{len(rows)} (sequence, kv head) rows of the decode step: anchor "
+                      f"geometry + merge + attention, {wall:.1f} s on one core"}
+
+
+def run_decode_bench(w, B, steps, warmup, cpu):
+    import torch
+    from paper_2607_21927_amd import ris
+    dev = torch.device("cuda:0")
+    G = w.Hq // w.Hkv
+    N = w.N
+    max_len = N + steps + warmup + 1
+    # Prompts of different lengths: sequence b generated its first token at
+    # N - 97 b, so the anchors differ between sequences.
+    t0s = [N - 97 * b for b in range(B)]
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(0)
+    Q = torch.randn(B, w.Hq, w.D, generator=gen, device=dev).to(torch.bfloat16)
+    K = torch.randn(B, w.Hkv, max_len, w.D, generator=gen, device=dev).to(torch.bfloat16)
+    V = torch.randn(B, w.Hkv, max_len, w.D, generator=gen, device=dev).to(torch.bfloat16)
+    md = ris.mask_desc(w.mode, w.density_ppm, max_len, w.Hkv, n_seeds=w.n_seeds, seed=w.seed,
+                       layer=0, block=w.block)
+    stride = max(ris.mask_rows_nnz_bound(md, t0, 1) for t0 in t0s)
+    aptr = torch.zeros(B * (w.Hkv + 1), dtype=torch.int64, device=dev)
+    aidx = torch.zeros(B * stride, dtype=torch.int32, device=dev)
+    a0, a1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a0.record()
+    for b, t0 in enumerate(t0s):
+        ris.mask_build_rows(md, t0, 1, aptr[b * (w.Hkv + 1):(b + 1) * (w.Hkv + 1)],
+                            aidx[b * stride:(b + 1) * stride], col_capacity=stride)
+    a1.record()
+    out = torch.empty(B, w.Hq, w.D, dtype=torch.bfloat16, device=dev)
+    dd = ris.decode_desc(Q, K, out, stride, window=w.window, sink=w.anchor)
+    ws = torch.empty(ris.decode_workspace_bytes(dd), dtype=torch.uint8, device=dev)
+    aptr_h, aidx_h = aptr.cpu().numpy(), aidx.cpu().numpy()
+    # Each step decodes the next token: position t0 + step.
+    positions = [torch.tensor([t0 + i for t0 in t0s], dtype=torch.int64, device=dev)
+                 for i in range(warmup + steps)]
+    pairs = sum(decode_pairs(aptr_h, aidx_h, stride, t0s, [t0 + warmup + i for t0 in t0s],
+                             w.Hkv, w.window, w.anchor) for i in range(steps))
+    for i in range(warmup):
+        ris.decode_attn(Q, K, V, positions[i], aptr, aidx, out, ws, dd)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for i in range(steps):
+        ris.decode_attn(Q, K, V, positions[warmup + i], aptr, aidx, out, ws, dd)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    kv_pairs = pairs / steps
+    achieved = kv_pairs * KV_PAIR_BYTES[w.D] / (ms * 1e-3) / 1e9
+    if cpu:
+        rows = [(0, 0), (B - 1, w.Hkv - 1)]
+        Kh = K[[b for b, _ in rows]].float().cpu().numpy()
+        cpu_res = cpu_decode_baseline(
+            w, [t0s[b] for b, _ in rows], [t0s[b] + warmup for b, _ in rows],
+            Q[[b for b, _ in rows]].float().cpu().numpy(), Kh,
+            V[[b for b, _ in rows]].float().cpu().numpy(), [(i, g) for i, (_, g) in enumerate(rows)])
+    else:
+        cpu_res = None
+    return {
+        "metric": "decode attended (q,k) pairs/s (Hybrid-Anchor step, batch of sequences)",
+        "value": kv_pairs * G / (ms * 1e-3),
+        "unit": "pairs/s",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic: Gaussian Q and K/V caches (torch.randn, seed 0)",
+        "config": {"workload": w.name + "_decode", "batch": B, "Hq": w.Hq, "Hkv": w.Hkv,
+                   "head_dim": w.D, "first_token_positions": f"{t0s[-1]}..{t0s[0]}",
+                   "density": w.density_ppm / 1e6, "seeds": w.n_seeds, "window": w.window,
+                   "sink": w.anchor},
+        "tokens_per_s": B / (ms * 1e-3),
+        "kv_pairs_per_step": kv_pairs,
+        "ms_anchor_build_once": a0.elapsed_time(a1),
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "kernel": "k_decode_partial", "bytes_per_kv_pair": KV_PAIR_BYTES[w.D]},
+        "cpu_baseline": cpu_res,
+    }
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -206,11 +326,19 @@ def main():
     ap.add_argument("--cpu-workers", type=int, default=16)
     ap.add_argument("--cpu-stride", type=int, default=64)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--decode", action="store_true",
+                    help="time the Hybrid-Anchor decode step instead of the prefill layer")
+    ap.add_argument("--batch", type=int, default=32, help="sequences per decode step")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: the hot path needs no cross-GPU exchange and this "
               "build has no multi-GPU launch (run with --gpus 1).", file=sys.stderr)
         sys.exit(2)
+    if args.decode:
+        wl = args.workload if args.workload != "qwen2_64k_stochastic_yarn" else "qwen2_64k_full_geometry"
+        print(json.dumps(run_decode_bench(WORKLOADS[wl], args.batch, args.steps, args.warmup,
+                                          not args.no_cpu_baseline)))
+        return
     w = WORKLOADS[args.workload]
     Q, K, V = gaussian_qkv(w.Hq, w.Hkv, w.N, w.D, seed=0)
 

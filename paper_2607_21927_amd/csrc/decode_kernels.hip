@@ -10,8 +10,9 @@
 // below the window.  Reading the three segments in turn is the unique()
 // merge without sorting, and no index is visited twice.
 //
-// Split-K: the list is cut into 256-key spans, one per wave (4 waves per
-// workgroup).  A wave runs a flash-style pass over 32-key tiles:
+// Split-K: the list is cut into 32-key tiles dealt round-robin to the P
+// waves of the row (4 waves per workgroup), so any row length is covered
+// whatever P the host picks.  A wave runs a flash-style pass over its tiles:
 //   * S^T = K Q^T on MFMA 16x16x32 bf16, K rows gathered straight from HBM
 //     into the A-operand layout (lane: key l%16, 8 dims at 8(l/16)), the G
 //     query heads of the group as the 16-wide MFMA dimension;
@@ -35,11 +36,8 @@ typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 typedef short s16x4_t __attribute__((ext_vector_type(4)));
 
-constexpr int kTileKeys = 32;
-constexpr int kWaveKeys = kDecodeChunkKeys / kDecodeWaves;
+constexpr int kTileKeys = kDecodeTileKeys;
 constexpr float kNegBig = -1e30f;   // finite start of the running max
-
-static_assert(kWaveKeys % kTileKeys == 0, "a wave span is whole tiles");
 
 // LDS transpose read (ds_read_b64_tr_b16): within each group of 16 lanes,
 // lane i receives element i mod 4 of what lanes 4e + i/4 (e = 0..3) address.
@@ -135,8 +133,7 @@ __global__ __launch_bounds__(64 * kDecodeWaves, 2) void k_decode_partial(DecodeP
         r.ns = p.sink < r.w_lo ? p.sink : r.w_lo;
     }
     const int64_t total = r.na + r.nw + r.ns;
-    const int64_t v_begin = part * kWaveKeys;
-    const int64_t v_end = total < v_begin + kWaveKeys ? total : v_begin + kWaveKeys;
+    const int64_t stride = (int64_t)p.parts * kTileKeys;   // this wave's tiles: part, part + P, ...
     const uint16_t* Kr = static_cast<const uint16_t*>(p.K) + (int64_t)row * p.max_len * D;
     const uint16_t* Vr = static_cast<const uint16_t*>(p.V) + (int64_t)row * p.max_len * D;
 
@@ -159,13 +156,14 @@ __global__ __launch_bounds__(64 * kDecodeWaves, 2) void k_decode_partial(DecodeP
     for (int db = 0; db < DB; ++db) o[db] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     float m_run = kNegBig, l_run = 0.f;
 
-    if (v_begin < v_end) {
+    const int64_t v_first = part * kTileKeys;
+    if (v_first < total) {
         KVTile<D> cur;
-        load_tile<D>(r, Kr, Vr, v_begin, li, lg, cur);
-        for (int64_t v0 = v_begin; v0 < v_end; v0 += kTileKeys) {
+        load_tile<D>(r, Kr, Vr, v_first, li, lg, cur);
+        for (int64_t v0 = v_first; v0 < total; v0 += stride) {
             KVTile<D> nxt;
-            const bool more = v0 + kTileKeys < v_end;
-            if (more) load_tile<D>(r, Kr, Vr, v0 + kTileKeys, li, lg, nxt);
+            const bool more = v0 + stride < total;
+            if (more) load_tile<D>(r, Kr, Vr, v0 + stride, li, lg, nxt);
 
             // V rows into this wave's LDS, row-major (key slot 16 kb + l%16).
 #pragma unroll
@@ -259,10 +257,14 @@ __global__ __launch_bounds__(64 * kDecodeWaves, 2) void k_decode_partial(DecodeP
     }
 }
 
-// Merge the partials of one (sequence, query head): one thread per dim.
+// Merge the partials of one (sequence, query head), one thread per dim: the
+// threads first find the common max and each partial's weight together (in
+// LDS), then every thread sums its dim over the partials.
 template <int D>
 __global__ __launch_bounds__(D) void k_decode_combine(DecodeParams p) {
-    const int d = threadIdx.x;
+    __shared__ float wgt[kDecodeMaxParts];
+    __shared__ float red[D / 64][2];
+    const int d = threadIdx.x, lane = d & 63, wv = d >> 6;
     const int64_t bh = blockIdx.x;
     const int b = (int)(bh / p.Hq), h = (int)(bh % p.Hq);
     const int g = h / p.G, hh = h - g * p.G;
@@ -271,13 +273,28 @@ __global__ __launch_bounds__(D) void k_decode_combine(DecodeParams p) {
     const float* ml = p.part_ml + row * p.parts * step_ml + 2 * hh;
     const float* po = p.part_o + row * p.parts * step_o + (int64_t)hh * D + d;
     float M = kNegBig;
-    for (int i = 0; i < p.parts; ++i) M = fmaxf(M, ml[i * step_ml]);
-    float L = 0.f, O = 0.f;
-    for (int i = 0; i < p.parts; ++i) {
+    for (int i = d; i < p.parts; i += D) M = fmaxf(M, ml[i * step_ml]);
+    M = wave_max(M);
+    if (lane == 0) red[wv][0] = M;
+    __syncthreads();
+    M = red[0][0];
+#pragma unroll
+    for (int w = 1; w < D / 64; ++w) M = fmaxf(M, red[w][0]);
+    float L = 0.f;
+    for (int i = d; i < p.parts; i += D) {
         const float w = __builtin_amdgcn_exp2f(ml[i * step_ml] - M);
+        wgt[i] = w;
         L += w * ml[i * step_ml + 1];
-        O += w * po[i * step_o];
     }
+    L = wave_sum(L);
+    if (lane == 0) red[wv][1] = L;
+    __syncthreads();
+    L = red[0][1];
+#pragma unroll
+    for (int w = 1; w < D / 64; ++w) L += red[w][1];
+    float O = 0.f;
+#pragma unroll 8
+    for (int i = 0; i < p.parts; ++i) O += wgt[i] * po[i * step_o];
     const float y = L > 0.f ? O / L : 0.f;
     const int64_t at = bh * D + d;
     if (p.out_bf16)
@@ -289,6 +306,7 @@ __global__ __launch_bounds__(D) void k_decode_combine(DecodeParams p) {
 template <int D>
 hipError_t launch_d(const DecodeParams& p, float c, hipStream_t st) {
     const dim3 grid((unsigned)(p.parts / kDecodeWaves), (unsigned)(p.B * p.Hkv));
+    if (p.parts % kDecodeWaves != 0 || p.parts > kDecodeMaxParts) return hipErrorInvalidValue;
     hipLaunchKernelGGL(k_decode_partial<D>, grid, dim3(64 * kDecodeWaves), 0, st, p, c);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;

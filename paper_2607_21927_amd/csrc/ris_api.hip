@@ -250,13 +250,22 @@ int ris_sparse_attn(const void* Q, const void* K, const void* V, const int64_t* 
 
 namespace {
 
+// Partials (waves) per row.  Any value covers every key (the tiles are dealt
+// round-robin); this one aims at ~2048 resident waves over the batch without
+// giving a wave less than one tile of a typical row (the anchor slice shared
+// evenly by the kv heads, plus window and initial tokens).
 int64_t decode_parts(const ris_decode_desc& d) {
     const int64_t win = d.window < d.max_len ? d.window : d.max_len;
     const int64_t snk = d.sink < d.max_len ? d.sink : d.max_len;
-    const int64_t keys = d.anchor_stride + win + snk;
-    int64_t chunks = (keys + ris::kDecodeChunkKeys - 1) / ris::kDecodeChunkKeys;
-    if (chunks < 1) chunks = 1;
-    return chunks * ris::kDecodeWaves;
+    const int64_t keys = (d.anchor_stride + d.Hkv - 1) / d.Hkv + win + snk;
+    const int64_t tiles = (keys + ris::kDecodeTileKeys - 1) / ris::kDecodeTileKeys;
+    const int64_t rows = (int64_t)d.batch * d.Hkv;
+    int64_t parts = (ris::kDecodeTargetWaves + rows - 1) / rows;
+    if (parts > tiles) parts = tiles;
+    parts = (parts + ris::kDecodeWaves - 1) / ris::kDecodeWaves * ris::kDecodeWaves;
+    if (parts < ris::kDecodeWaves) parts = ris::kDecodeWaves;
+    if (parts > ris::kDecodeMaxParts) parts = ris::kDecodeMaxParts;
+    return parts;
 }
 
 int validate_decode(const ris_decode_desc* d) {
@@ -274,7 +283,6 @@ int validate_decode(const ris_decode_desc* d) {
     if (!(d->scale >= 0.0f) || !isfinite(d->scale)) return RIS_E_ARG;
     if ((int64_t)d->batch * d->Hkv > 65535) return RIS_E_UNSUPPORTED;
     if ((int64_t)d->batch * d->Hq > 0x7FFFFFFFll) return RIS_E_UNSUPPORTED;
-    if (decode_parts(*d) > (1ll << 30)) return RIS_E_UNSUPPORTED;
     return RIS_OK;
 }
 

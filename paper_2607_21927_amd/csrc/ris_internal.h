@@ -68,11 +68,14 @@ __device__ __forceinline__ bool tile_is_dense(const AttnParams& a, int g, int64_
 hipError_t launch_attn_gather(const AttnParams& a, hipStream_t st);
 hipError_t launch_attn_tile(const AttnParams& a, hipStream_t st);
 
-// Decode step (Hybrid Anchor).  A workgroup of kDecodeWaves waves covers
-// kDecodeChunkKeys keys of one row's virtual key list; every wave writes one
-// partial (its max, sum and unnormalised output per head).
+// Decode step (Hybrid Anchor).  Each row's virtual key list is cut into
+// kDecodeTileKeys-key tiles dealt round-robin to the row's `parts` waves
+// (kDecodeWaves per workgroup); every wave writes one partial (its max, sum
+// and unnormalised output per head).
 constexpr int kDecodeWaves = 4;
-constexpr int kDecodeChunkKeys = 1024;
+constexpr int kDecodeTileKeys = 32;
+constexpr int kDecodeMaxParts = 1024;
+constexpr int kDecodeTargetWaves = 2048;   // 256 CUs x 8 resident waves
 struct DecodeParams {
     const void* Q;                // [B, Hq, D] bf16
     const void* K;                // [B, Hkv, max_len, D] bf16

@@ -184,9 +184,11 @@ def test_decode_validation(ris, bad, code):
 
 def test_decode_workspace_size_and_capacity_error(ris):
     d = _decode(ris)
-    # 2 sequences x 2 kv heads x 8 partials (1000 + 1024 + 4 keys -> 2 chunks
-    # of 1024 keys, 4 waves each) x 6 heads x (128 + 2) floats
-    assert ris.decode_workspace_bytes(d) == 2 * 2 * 8 * 6 * 130 * 4
+    # 2 sequences x 2 kv heads x 48 partials (a row of ~500 + 1024 + 4 keys
+    # is 48 tiles of 32; 2048 waves / 4 rows would be 512) x 6 heads x
+    # (128 + 2) floats
+    assert ris.decode_workspace_bytes(d) == 2 * 2 * 48 * 6 * 130 * 4
+    assert ris.decode_workspace_bytes(_decode(ris, batch=64)) == 64 * 2 * 16 * 6 * 130 * 4
     L = ris.lib()
     f = ctypes.c_void_p(0x1000)
     need = ris.decode_workspace_bytes(d)

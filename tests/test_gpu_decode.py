@@ -199,3 +199,16 @@ def test_decode_full_size_qwen2_64k():
     err = float(np.abs(got - want).max())
     say(f"  full-size decode max err {err:.3e}")
     assert err <= 2e-2
+
+
+def test_decode_large_batch_many_tiles_per_wave():
+    """64 sequences x 2 kv heads: few waves per row, so every wave walks
+    several 32-key tiles (the round-robin split and the prefetch chain)."""
+    B = 64
+    t0s = [3000 + 13 * b for b in range(B)]
+    ts = [t0 + (b % 5) * 40 for b, t0 in enumerate(t0s)]
+    got, want, vmax = run_decode(12, 2, 128, 0, 10_000, 10, 0, 1024, 4, t0s, ts, 4100, "f32",
+                                 check_anchor=False)
+    err = float(np.abs(got - want).max())
+    say(f"  batch-64 decode max err {err:.3e}")
+    assert err <= tight_tol(vmax)
