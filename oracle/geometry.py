@@ -140,7 +140,7 @@ def row_sets(spec, kv_head, qs):
     S = spec.n_seeds
     seeds = (np.uint64(spec.seed) + np.arange(S, dtype=np.uint64))
     rk = philox.row_round_keys(seeds[None, :], qs[:, None].astype(np.uint64),
-                               np.uint64(kv_head), np.uint64(spec.layer))   # (R, S, 6)
+                               np.uint64(kv_head), np.uint64(spec.layer))   # (R, S, 8)
     per_row = kk * S
     total = int(per_row.sum())
     ri = np.repeat(np.arange(len(qs)), per_row)

@@ -12,8 +12,8 @@ independently, in any order, on either side of the parity check.
 
 Reading taken here: the row key is derived from Philox with
 ``key = (seed, 0)`` and ``counter = (query, kv_head, layer, 0)``; the four
-64-bit outputs are split into eight 32-bit words, low half first, and the first
-six become the six Feistel round keys.
+64-bit outputs are split into eight 32-bit words, low half first, which feed
+the Feistel round keys (see ``prp``).
 
 Pinned by: known-answer equality with ``numpy.random.Philox`` (an independent
 library implementation of the same published algorithm).
@@ -73,9 +73,9 @@ def philox4x64_10(counter, key):
 
 
 def row_round_keys(seed, q, kv_head, layer):
-    """Six 32-bit Feistel round keys for one (seed, layer, kv_head, query) row.
+    """The eight 32-bit words of one (seed, layer, kv_head, query) row.
 
-    All arguments broadcast.  Returns a uint64 array of shape (..., 6) whose
+    All arguments broadcast.  Returns a uint64 array of shape (..., 8) whose
     values are < 2**32.
     """
     seed = np.asarray(seed, dtype=np.uint64)
@@ -85,7 +85,7 @@ def row_round_keys(seed, q, kv_head, layer):
         (seed, np.uint64(0)),
     )
     words = []
-    for w in o[:3]:
+    for w in o:
         words.append(w & _LO32)
         words.append(w >> _S32)
     return np.stack(words, axis=-1)

@@ -8,19 +8,34 @@ pool -- so that the density is met exactly per row and no per-seed dedupe is
 needed.  It is realised by a keyed pseudo-random permutation ``P`` of
 ``[0, n)`` and taking ``{P(0), ..., P(k-1)}``.
 
-``P`` is a balanced Feistel network on ``m``-bit words,
-``m = max(2, bitlen(n-1))`` rounded up to even, half width ``h = m/2``, six
-rounds.  Round ``r`` maps ``(L, R) -> (R, L xor (F(R xor rk_r) & (2^h-1)))``
-with ``F`` the MurmurHash3 32-bit finaliser ``fmix32`` (Appleby, public
-domain).  Values ``>= n`` are cycle-walked (re-encrypted until they fall in
-range), which restricts a permutation of ``[0, 2^m)`` to one of ``[0, n)``
-(Black and Rogaway, "Ciphers with arbitrary finite domains", 2002).
+``P`` is a Feistel network on ``m``-bit words with MurmurHash3's 32-bit
+finaliser ``fmix32`` (Appleby, public domain) as round function:
+
+* width: ``m0 = max(2, bitlen(n-1))``; below 6 bits it is rounded up to even
+  (``m`` = 2, 4 or 6), from 6 bits on ``m = m0`` -- the smallest power-of-two
+  domain that holds the pool, so that cycle walking takes fewer than two
+  evaluations per draw on average;
+* halves: left ``a = floor(m/2)`` bits (high), right ``b = m - a`` bits (low);
+  a round replaces the left half, ``(L, R) -> (R, L xor (F(R xor k_r) mod 2^|L|))``,
+  so the half widths alternate (a, b), (b, a), ... and an even round count
+  returns to (a, b) -- the alternating split of FFX / NIST FF1 for odd widths;
+* rounds: 6 for ``m >= 6`` (halves of at least 3 bits), 12 for ``m`` = 2 or 4,
+  where 1- and 2-bit halves mix slowly;
+* round keys: ``k_r = w_r`` for ``r < 8`` and ``k_r = w_{r-8} xor 0x9E3779B9``
+  for ``r = 8..11``, with ``w`` the eight 32-bit words of the row's Philox
+  output.
+
+Values ``>= n`` are cycle-walked (re-encrypted until they fall in range),
+which restricts a permutation of ``[0, 2^m)`` to one of ``[0, n)`` (Black and
+Rogaway, "Ciphers with arbitrary finite domains", 2002).
 
 Pinned by: ``fmix32`` against scikit-learn's MurmurHash3 of the empty string
-(which reduces to ``fmix32(seed)``); exhaustive bijectivity; distinctness and
-range of cycle-walked draws; chi-square uniformity of inclusion over keys.
-The particular permutation is a definitional choice (any uniform draw realises
-the paper's sampling); the GPU reproduces it bit for bit.
+(which reduces to ``fmix32(seed)``); exhaustive bijectivity for every width up
+to 16 bits; distinctness and range of cycle-walked draws; chi-square
+uniformity over independent keys of inclusion, of the first draw and of the
+ordered pair (P(0), P(1)).  The particular permutation is a definitional
+choice (any uniform draw realises the paper's sampling); the GPU reproduces it
+bit for bit.
 """
 
 import numpy as np
@@ -28,7 +43,8 @@ import numpy as np
 _M32 = np.uint64(0xFFFFFFFF)
 FMIX_C1 = np.uint64(0x85EBCA6B)
 FMIX_C2 = np.uint64(0xC2B2AE35)
-ROUNDS = 6
+KEY_TWEAK = np.uint64(0x9E3779B9)
+WORDS = 8          # row words (round-key material)
 
 
 def fmix32(h):
@@ -43,10 +59,8 @@ def fmix32(h):
 
 
 def domain_bits(n):
-    """Feistel word width m for pool sizes n (even, at least 2).
-
-    Works elementwise on integer arrays; n = 1 gives 2 (unused: P is 0 there).
-    """
+    """Word width m for pool sizes n (elementwise): max(2, bitlen(n-1)),
+    rounded up to even below 6.  n = 1 gives 2 (unused: P is 0 there)."""
     n = np.asarray(n, dtype=np.int64)
     m = np.zeros(n.shape, dtype=np.int64)
     v = np.maximum(n - 1, 0)
@@ -54,46 +68,67 @@ def domain_bits(n):
         m += (v > 0)
         v >>= 1
     m = np.maximum(m, 2)
-    return m + (m & 1)
+    return np.where(m < 6, m + (m & 1), m)
 
 
-def feistel(x, rk, m):
-    """One application of the six-round Feistel permutation of [0, 2^m).
+def rounds(m):
+    """Round count for width m (a scalar)."""
+    return 6 if m >= 6 else 12
 
-    x: uint64 array of values < 2^m.  rk: uint64 array (..., 6) of round keys
-    with leading shape equal to x's.  m: even word widths, broadcast with x.
+
+def round_key(w, r):
+    """k_r from the row words w (..., 8)."""
+    return w[..., r] if r < WORDS else (w[..., r - WORDS] ^ KEY_TWEAK)
+
+
+def feistel(x, w, m):
+    """One application of the keyed permutation of [0, 2^m) for one width m.
+
+    x: uint64 array of values < 2^m.  w: uint64 array (..., 8) of row words
+    with leading shape equal to x's.  m: a scalar width from domain_bits.
     """
     x = np.asarray(x, dtype=np.uint64)
-    h = np.broadcast_to(np.asarray(m, dtype=np.uint64) // np.uint64(2), x.shape)
-    mask = (np.uint64(1) << h) - np.uint64(1)
-    left = x >> h
-    right = x & mask
-    for r in range(ROUNDS):
-        f = fmix32(right ^ rk[..., r]) & mask
+    a = m // 2
+    b = m - a
+    left = x >> np.uint64(b)
+    right = x & np.uint64((1 << b) - 1)
+    wl, wr = a, b
+    for r in range(rounds(m)):
+        f = fmix32(right ^ round_key(w, r)) & np.uint64((1 << wl) - 1)
         left, right = right, left ^ f
-    return (left << h) | right
+        wl, wr = wr, wl
+    return (left << np.uint64(wr)) | right
 
 
-def permute(j, rk, n):
+def _feistel_by_width(x, w, m):
+    """feistel over arrays whose widths m differ element by element."""
+    out = np.empty_like(x)
+    for mm in np.unique(m):
+        sel = m == mm
+        out[sel] = feistel(x[sel], w[sel], int(mm))
+    return out
+
+
+def permute(j, w, n):
     """P(j) for the keyed permutation of [0, n), by cycle walking.
 
-    j: uint64 array of values < n.  rk: round keys (j.shape + (6,)) or one key
-    set (6,).  n: pool sizes >= 1, broadcast with j.
+    j: uint64 array of values < n.  w: row words (j.shape + (8,)) or one word
+    set (8,).  n: pool sizes >= 1, broadcast with j.
     """
     j = np.asarray(j, dtype=np.uint64)
     n = np.broadcast_to(np.asarray(n, dtype=np.uint64), j.shape)
-    rk = np.broadcast_to(np.asarray(rk, dtype=np.uint64), j.shape + (ROUNDS,))
+    w = np.broadcast_to(np.asarray(w, dtype=np.uint64), j.shape + (WORDS,))
     m = domain_bits(n.astype(np.int64))
-    x = feistel(j, rk, m)
+    x = _feistel_by_width(j, w, m)
     bad = x >= n
     while bad.any():
-        x[bad] = feistel(x[bad], rk[bad], m[bad])
+        x[bad] = _feistel_by_width(x[bad], w[bad], m[bad])
         bad = x >= n
     return np.where(n == np.uint64(1), np.uint64(0), x)
 
 
-def draw(k, n, rk):
+def draw(k, n, w):
     """The k keys {P(0), ..., P(k-1)} drawn from [0, n) (distinct, unsorted)."""
     if k <= 0 or n <= 0:
         return np.zeros(0, dtype=np.uint64)
-    return permute(np.arange(k, dtype=np.uint64), np.asarray(rk, dtype=np.uint64), n)
+    return permute(np.arange(k, dtype=np.uint64), np.asarray(w, dtype=np.uint64), n)

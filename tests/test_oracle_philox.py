@@ -48,17 +48,17 @@ def test_block_matches_numpy(case):
 
 
 def test_row_round_keys_layout():
-    """Six round keys = the first three 64-bit outputs split low half first,
+    """Eight row words = the four 64-bit outputs split low half first,
     for key (seed, 0) and counter (q, kv_head, layer, 0); vectorised calls agree
     with scalar ones."""
     seeds = np.array([0, 1, 69, 2**40 + 3], dtype=np.uint64)
     qs = np.array([0, 1, 511, 65535], dtype=np.uint64)
     rk = philox.row_round_keys(seeds[None, :], qs[:, None], np.uint64(1), np.uint64(7))
-    assert rk.shape == (4, 4, 6)
+    assert rk.shape == (4, 4, 8)
     for a, q in enumerate(qs):
         for b, s in enumerate(seeds):
             out = numpy_block([int(q), 1, 7, 0], [int(s), 0])
             words = []
-            for w in out[:3]:
+            for w in out:
                 words += [w & 0xFFFFFFFF, w >> 32]
             assert [int(x) for x in rk[a, b]] == words

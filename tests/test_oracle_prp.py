@@ -1,6 +1,7 @@
 """Pins for the oracle's exact-k draw (see oracle/prp.py)."""
 import numpy as np
 import pytest
+from scipy.stats import chi2
 from sklearn.utils import murmurhash3_32
 
 from oracle import prp
@@ -17,28 +18,59 @@ def test_fmix32_against_sklearn_murmurhash3():
     assert int(prp.fmix32(np.uint64(1))) == 0x514E28B7   # published test vector
 
 
-def test_domain_bits():
-    ns = [1, 2, 3, 4, 5, 8, 9, 16, 17, 64, 65, 4096, 4097, 65536, 65537]
-    want = [2, 2, 2, 2, 4, 4, 4, 4, 6, 6, 8, 12, 14, 16, 18]
+def test_domain_bits_and_rounds():
+    ns = [1, 2, 3, 4, 5, 8, 9, 16, 17, 32, 33, 64, 65, 4096, 4097, 65536, 65537, 262144]
+    want = [2, 2, 2, 2, 4, 4, 4, 4, 6, 6, 6, 6, 7, 12, 13, 16, 17, 18]
     assert list(prp.domain_bits(np.array(ns))) == want
+    assert [prp.rounds(m) for m in (2, 4, 6, 7, 18)] == [12, 12, 6, 6, 6]
+    # the domain never exceeds twice the pool once the width is exact (n > 32)
+    for n in [33, 100, 1000, 65536, 65537, 262144]:
+        assert (1 << int(prp.domain_bits(n))) < 2 * n
 
 
-@pytest.mark.parametrize("m", [2, 4, 6, 8, 10, 12, 14, 16])
+def test_feistel_matches_a_plain_python_rewrite():
+    """The vectorised rounds equal a scalar rewrite of the stated network."""
+    rng = np.random.default_rng(7)
+    M = 0xFFFFFFFF
+
+    def fmix(h):
+        h ^= h >> 16
+        h = (h * 0x85EBCA6B) & M
+        h ^= h >> 13
+        h = (h * 0xC2B2AE35) & M
+        return h ^ (h >> 16)
+
+    for m in [2, 4, 6, 7, 9, 16, 17]:
+        w = [int(v) for v in rng.integers(0, 2**32, size=8, dtype=np.uint64)]
+        xs = rng.integers(0, 1 << m, size=40, dtype=np.uint64)
+        got = prp.feistel(xs, np.broadcast_to(np.array(w, dtype=np.uint64), (40, 8)), m)
+        a, b = m // 2, m - m // 2
+        for x, g in zip(xs, got):
+            left, right, wl = int(x) >> b, int(x) & ((1 << b) - 1), a
+            for r in range(12 if m < 6 else 6):
+                k = w[r] if r < 8 else w[r - 8] ^ 0x9E3779B9
+                f = fmix(right ^ k) & ((1 << wl) - 1)
+                left, right = right, left ^ f
+                wl = b if wl == a and r % 2 == 0 else a
+            assert ((left << b) | right) == int(g)
+
+
+@pytest.mark.parametrize("m", [2, 4, 6, 7, 8, 9, 10, 11, 12, 13, 14, 15, 16])
 def test_feistel_is_a_bijection(m):
     rng = np.random.default_rng(m)
-    for _ in range(2 if m == 16 else 4):
-        rk = rng.integers(0, 2**32, size=6, dtype=np.uint64)
+    for _ in range(2 if m >= 15 else 4):
+        w = rng.integers(0, 2**32, size=8, dtype=np.uint64)
         x = np.arange(1 << m, dtype=np.uint64)
-        y = prp.feistel(x, np.broadcast_to(rk, x.shape + (6,)), m)
+        y = prp.feistel(x, np.broadcast_to(w, x.shape + (8,)), m)
         assert y.max() < (1 << m)
         assert np.unique(y).size == (1 << m)
 
 
-@pytest.mark.parametrize("n", [1, 2, 3, 5, 7, 17, 100, 257, 1000, 4097, 40000])
+@pytest.mark.parametrize("n", [1, 2, 3, 5, 7, 17, 33, 100, 257, 1000, 4097, 40000])
 def test_cycle_walk_permutes_the_pool(n):
     rng = np.random.default_rng(n)
-    rk = rng.integers(0, 2**32, size=6, dtype=np.uint64)
-    y = prp.permute(np.arange(n, dtype=np.uint64), rk, n)
+    w = rng.integers(0, 2**32, size=8, dtype=np.uint64)
+    y = prp.permute(np.arange(n, dtype=np.uint64), w, n)
     assert np.array_equal(np.sort(y), np.arange(n, dtype=np.uint64))
 
 
@@ -46,27 +78,61 @@ def test_draw_is_distinct_and_in_range():
     rng = np.random.default_rng(3)
     for n in [1, 2, 9, 333, 5000]:
         for k in [1, n // 3 + 1, n]:
-            rk = rng.integers(0, 2**32, size=6, dtype=np.uint64)
-            d = prp.draw(k, n, rk)
+            w = rng.integers(0, 2**32, size=8, dtype=np.uint64)
+            d = prp.draw(k, n, w)
             assert d.size == k and np.unique(d).size == k and d.max() < n
 
 
-@pytest.mark.parametrize("n,k", [(7, 3), (13, 1), (33, 10)])
-def test_inclusion_is_uniform(n, k):
-    """Over many independent keys each pool element is drawn with
-    probability k/n (chi-square, 1e-4 false-alarm level)."""
-    from scipy.stats import chi2
-    rng = np.random.default_rng(n * 100 + k)
-    trials = 6000
-    keys = rng.integers(0, 2**32, size=(trials, 6), dtype=np.uint64)
+def _draws(n, k, trials, seed):
+    keys = np.random.default_rng(seed).integers(0, 2**32, size=(trials, 8), dtype=np.uint64)
     j = np.tile(np.arange(k, dtype=np.uint64), trials)
-    x = prp.permute(j, np.repeat(keys, k, axis=0), n)
-    counts = np.bincount(x.astype(np.int64), minlength=n)
-    expect = trials * k / n
-    stat = float(((counts - expect) ** 2 / expect).sum())
-    assert stat < chi2.ppf(1 - 1e-4, n - 1)
-    # the first drawn key is uniform as well (no bias toward small values)
-    first = x.reshape(trials, k)[:, 0].astype(np.int64)
-    c1 = np.bincount(first, minlength=n)
-    e1 = trials / n
-    assert float(((c1 - e1) ** 2 / e1).sum()) < chi2.ppf(1 - 1e-4, n - 1)
+    return prp.permute(j, np.repeat(keys, k, axis=0), n).astype(np.int64).reshape(trials, k)
+
+
+def _chi2_ok(obs, expect, df):
+    stat = float(((obs - expect) ** 2 / expect).sum())
+    return stat < chi2.ppf(1 - 1e-4, df), stat
+
+
+@pytest.mark.parametrize("n,k", [(5, 2), (7, 3), (13, 1), (33, 10), (65, 6), (300, 20)])
+def test_inclusion_and_first_draw_are_uniform(n, k):
+    """Over many independent keys each pool element is drawn with
+    probability k/n, and the first drawn key is uniform (chi-square, 1e-4
+    false-alarm level)."""
+    trials = 20000
+    x = _draws(n, k, trials, n * 100 + k)
+    ok, stat = _chi2_ok(np.bincount(x.ravel(), minlength=n), trials * k / n, n - 1)
+    assert ok, stat
+    ok, stat = _chi2_ok(np.bincount(x[:, 0], minlength=n), trials / n, n - 1)
+    assert ok, stat
+
+
+@pytest.mark.parametrize("n", [4, 5, 7, 9, 16, 17, 32, 33, 65])
+def test_successive_draws_are_jointly_uniform(n):
+    """(P(0), P(1)) is uniform over ordered pairs of distinct keys, one pair
+    per independent key (so the cells are a true multinomial); widths with
+    1- and 2-bit halves (n <= 16) included."""
+    trials = max(40000, 25 * n * (n - 1))
+    x = _draws(n, 2, trials, 1000 + n)
+    counts = np.bincount(x[:, 0] * n + x[:, 1], minlength=n * n).reshape(n, n)
+    off = ~np.eye(n, dtype=bool)
+    assert counts[~off].sum() == 0
+    ok, stat = _chi2_ok(counts[off], trials / (n * (n - 1)), n * (n - 1) - 1)
+    assert ok, stat
+
+
+def test_walk_needs_fewer_than_two_evaluations_per_draw():
+    """With a power-of-two domain below twice the pool the cycle walk averages
+    fewer than two permutation evaluations per draw."""
+    rng = np.random.default_rng(11)
+    for n in [33, 600, 5000, 40000, 65537]:
+        w = rng.integers(0, 2**32, size=8, dtype=np.uint64)
+        m = int(prp.domain_bits(n))
+        x = np.arange(n, dtype=np.uint64)
+        steps = np.ones(n)
+        y = prp.feistel(x, np.broadcast_to(w, (n, 8)), m)
+        while (y >= n).any():
+            bad = y >= n
+            steps[bad] += 1
+            y[bad] = prp.feistel(y[bad], np.broadcast_to(w, (int(bad.sum()), 8)), m)
+        assert steps.mean() < 2.0
