@@ -20,7 +20,7 @@ namespace ris {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kSeedBatch = 256;  // round keys of this many seeds live in LDS at once
+constexpr int kSeedBatch = 256;  // row words of this many seeds live in LDS at once
 
 struct RowGeom {
     uint32_t pool;          // draw pool [0, pool)
@@ -61,6 +61,44 @@ __device__ __forceinline__ void split_draw(uint32_t idx, uint32_t draws, float i
     if (j >= (int)draws) { ++s; j -= (int)draws; }
 }
 
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+
+// One lane's share of the batch's (seed, draw) pairs, OR-ed into the bitmap.
+// Each lane walks its draws one permutation step per iteration: a lane whose
+// value lands in the pool emits it and starts its next draw at once, so cycle
+// walks of different lengths do not hold the wave at the slowest lane.  Every
+// walk ends within the domain size (the cycle through j < n returns to j);
+// the step bound only makes that explicit.
+template <int ROUNDS>
+__device__ __forceinline__ void walk_draws(const FeistelDomain& dom, const uint32_t* rks,
+                                           uint32_t* bits, uint32_t total, uint32_t draws,
+                                           float inv_draws) {
+    uint32_t idx = threadIdx.x;
+    uint32_t x = 0, steps = 0;
+    uint32_t w[kRowWords];
+    auto start = [&]() {
+        int s, j;
+        split_draw(idx, draws, inv_draws, s, j);
+        x = (uint32_t)j;
+        const u32x4_t w0 = *reinterpret_cast<const u32x4_t*>(&rks[s * kRowWords]);
+        const u32x4_t w1 = *reinterpret_cast<const u32x4_t*>(&rks[s * kRowWords + 4]);
+        w[0] = w0.x; w[1] = w0.y; w[2] = w0.z; w[3] = w0.w;
+        w[4] = w1.x; w[5] = w1.y; w[6] = w1.z; w[7] = w1.w;
+    };
+    if (idx < total) start();
+    while (idx < total) {
+        x = feistel<ROUNDS>(x, w, dom.a, dom.b);
+        ++steps;
+        if (x < dom.n || steps >= dom.size) {
+            if (x >= dom.n) x = 0;
+            atomicOr(&bits[x >> 5], 1u << (x & 31u));
+            idx += kThreads;
+            steps = 0;
+            if (idx < total) start();
+        }
+    }
+}
+
 // Bits [lo, hi) that fall in word w.
 __device__ __forceinline__ uint32_t range_bits(uint32_t w, uint32_t lo, uint32_t hi) {
     const uint32_t b0 = w * 32u, b1 = b0 + 32u;
@@ -96,47 +134,19 @@ __device__ void build_row_bitmap(const MaskParams& p, int64_t q, int h, const Ro
     for (int s0 = 0; s0 < p.n_seeds; s0 += batch) {
         const int sb = min(batch, p.n_seeds - s0);
         __syncthreads();   // bitmap cleared / previous batch's keys no longer read
-        // Round keys of the batch's seeds, one Philox evaluation per lane.
+        // Row words of the batch's seeds, one Philox evaluation per lane.
         for (int t = tid; t < sb; t += kThreads) {
-            uint32_t rk[6];
-            row_round_keys(p.seed + (uint64_t)(s0 + t), (uint64_t)q, (uint64_t)h, (uint64_t)p.layer, rk);
-#pragma unroll
-            for (int e = 0; e < 6; ++e) rks[t * 6 + e] = rk[e];
+            uint32_t w[kRowWords];
+            row_round_keys(p.seed + (uint64_t)(s0 + t), (uint64_t)q, (uint64_t)h, (uint64_t)p.layer, w);
+            *reinterpret_cast<u32x4_t*>(&rks[t * kRowWords]) = u32x4_t{w[0], w[1], w[2], w[3]};
+            *reinterpret_cast<u32x4_t*>(&rks[t * kRowWords + 4]) = u32x4_t{w[4], w[5], w[6], w[7]};
         }
         __syncthreads();
-        // Each lane walks its draws one permutation step per iteration: a lane
-        // whose value lands in the pool emits it and starts its next draw at
-        // once, so cycle walks of different lengths do not hold the wave at
-        // the slowest lane.  Every walk ends within the domain size (the cycle
-        // through j < n returns to j); the step bound only makes that explicit.
         const uint32_t total = (uint32_t)sb * g.draws;
-        uint32_t idx = tid;
-        uint32_t x = 0, steps = 0;
-        uint32_t rk[6];
-        if (idx < total) {
-            int s, j;
-            split_draw(idx, g.draws, inv_draws, s, j);
-            x = (uint32_t)j;
-#pragma unroll
-            for (int e = 0; e < 6; ++e) rk[e] = rks[s * 6 + e];
-        }
-        while (idx < total) {
-            x = feistel6(x, rk, dom.half, dom.mask);
-            ++steps;
-            if (x < dom.n || steps >= dom.size) {
-                if (x >= dom.n) x = 0;
-                atomicOr(&bits[x >> 5], 1u << (x & 31u));
-                idx += kThreads;
-                steps = 0;
-                if (idx < total) {
-                    int s, j;
-                    split_draw(idx, g.draws, inv_draws, s, j);
-                    x = (uint32_t)j;
-#pragma unroll
-                    for (int e = 0; e < 6; ++e) rk[e] = rks[s * 6 + e];
-                }
-            }
-        }
+        if (dom.rounds == 6)
+            walk_draws<6>(dom, rks, bits, total, g.draws, inv_draws);
+        else
+            walk_draws<12>(dom, rks, bits, total, g.draws, inv_draws);
     }
     __syncthreads();
 }
@@ -174,10 +184,10 @@ __device__ __forceinline__ void row_of_block(const MaskParams& p, int64_t& r, in
 }
 
 __global__ __launch_bounds__(kThreads) void k_mask_count(MaskParams p, int64_t* row_ptr) {
-    extern __shared__ uint32_t smem[];
+    extern __shared__ __align__(16) uint32_t smem[];
     __shared__ uint32_t red[4];
     uint32_t* rks = smem;
-    uint32_t* bits = smem + kSeedBatch * 6;
+    uint32_t* bits = smem + kSeedBatch * kRowWords;
     int64_t r, q; int h;
     row_of_block(p, r, q, h);
     const RowGeom g = row_geometry(p, q);
@@ -191,10 +201,10 @@ __global__ __launch_bounds__(kThreads) void k_mask_count(MaskParams p, int64_t* 
 
 __global__ __launch_bounds__(kThreads) void k_mask_fill(MaskParams p, const int64_t* row_ptr,
                                                         int32_t* col_idx, int64_t capacity) {
-    extern __shared__ uint32_t smem[];
+    extern __shared__ __align__(16) uint32_t smem[];
     __shared__ uint32_t red[4];
     uint32_t* rks = smem;
-    uint32_t* bits = smem + kSeedBatch * 6;
+    uint32_t* bits = smem + kSeedBatch * kRowWords;
     int64_t r, q; int h;
     row_of_block(p, r, q, h);
     const int64_t base = row_ptr[r];
@@ -252,11 +262,11 @@ __device__ __forceinline__ void status_store(int64_t* p, int64_t v) {
 
 __global__ __launch_bounds__(kThreads) void k_mask_fused(MaskParams p, int64_t* row_ptr,
                                                          int32_t* col_idx, int64_t capacity) {
-    extern __shared__ uint32_t smem[];
+    extern __shared__ __align__(16) uint32_t smem[];
     __shared__ uint32_t red[4];
     __shared__ int64_t s_ticket, s_base;
     uint32_t* rks = smem;
-    uint32_t* bits = smem + kSeedBatch * 6;
+    uint32_t* bits = smem + kSeedBatch * kRowWords;
     const int64_t R = (int64_t)p.heads * p.nq;
     if (threadIdx.x == 0) {
         const int64_t t = (int64_t)atomicAdd(reinterpret_cast<unsigned long long*>(row_ptr), 1ull);
@@ -391,7 +401,7 @@ size_t mask_smem_bytes(const MaskParams& p) {
     // Largest pool of the built rows: q0 + nq keys (causal) or N.
     const int64_t span = p.causal ? p.q0 + p.nq : p.N;
     const int64_t words = (span + 31) / 32;
-    return (size_t)(kSeedBatch * 6 + words) * sizeof(uint32_t);
+    return (size_t)(kSeedBatch * kRowWords + words) * sizeof(uint32_t);
 }
 
 }  // namespace

@@ -30,15 +30,16 @@ __device__ __forceinline__ Philox4x64Out philox4x64_10(uint64_t c0, uint64_t c1,
     return o;
 }
 
-// Six 32-bit round keys of one row: the first three Philox outputs, low word
-// first; key = (seed, 0), counter = (q, kv_head, layer, 0).
+// The eight 32-bit words of one row (round-key material): the four Philox
+// outputs, low word first; key = (seed, 0), counter = (q, kv_head, layer, 0).
+constexpr int kRowWords = 8;
 __device__ __forceinline__ void row_round_keys(uint64_t seed, uint64_t q, uint64_t kv_head,
-                                               uint64_t layer, uint32_t rk[6]) {
+                                               uint64_t layer, uint32_t w[kRowWords]) {
     const Philox4x64Out o = philox4x64_10(q, kv_head, layer, 0ull, seed, 0ull);
 #pragma unroll
-    for (int i = 0; i < 3; ++i) {
-        rk[2 * i] = (uint32_t)o.v[i];
-        rk[2 * i + 1] = (uint32_t)(o.v[i] >> 32);
+    for (int i = 0; i < 4; ++i) {
+        w[2 * i] = (uint32_t)o.v[i];
+        w[2 * i + 1] = (uint32_t)(o.v[i] >> 32);
     }
 }
 
@@ -50,44 +51,46 @@ __device__ __forceinline__ uint32_t fmix32(uint32_t h) {
     return h;
 }
 
-// Keyed permutation of [0, n) used for exact-k draws: balanced six-round
-// Feistel network on m-bit words (m even, h = m/2) restricted to [0, n) by
-// cycle walking.
+// Keyed permutation of [0, n) used for exact-k draws: a Feistel network on
+// m-bit words with fmix32 rounds, restricted to [0, n) by cycle walking.
+// m = max(2, bitlen(n - 1)), rounded up to even below 6 bits; left half
+// a = m/2 bits (high), right half b = m - a (low); each round replaces the
+// left half, so the widths alternate (a, b), (b, a), ...; 6 rounds from 6 bits
+// on, 12 below.  Round key r is word r, or word r - 8 xor 0x9E3779B9.
 struct FeistelDomain {
-    uint32_t n;      // pool size (>= 1)
-    uint32_t half;   // h
-    uint32_t mask;   // 2^h - 1
-    uint32_t size;   // 2^m
+    uint32_t n;       // pool size (>= 1)
+    uint32_t a, b;    // left / right half widths
+    uint32_t rounds;  // 6 or 12
+    uint32_t size;    // 2^m
 };
 
 __host__ __device__ __forceinline__ FeistelDomain make_domain(uint32_t n) {
     uint32_t bits = 0;
     for (uint32_t v = n > 0 ? n - 1 : 0; v; v >>= 1) ++bits;
     if (bits < 2) bits = 2;
-    bits += bits & 1u;
+    if (bits < 6) bits += bits & 1u;
     FeistelDomain d;
-    d.n = n; d.half = bits / 2; d.mask = (1u << d.half) - 1u; d.size = 1u << bits;
+    d.n = n; d.a = bits / 2; d.b = bits - d.a;
+    d.rounds = bits >= 6 ? 6u : 12u;
+    d.size = 1u << bits;
     return d;
 }
 
-__device__ __forceinline__ uint32_t feistel6(uint32_t x, const uint32_t rk[6], uint32_t half,
-                                             uint32_t mask) {
-    uint32_t L = x >> half, R = x & mask;
+constexpr uint32_t kKeyTweak = 0x9E3779B9u;
+
+template <int ROUNDS>
+__device__ __forceinline__ uint32_t feistel(uint32_t x, const uint32_t w[kRowWords], uint32_t a,
+                                            uint32_t b) {
+    uint32_t L = x >> b, R = x & ((1u << b) - 1u);
 #pragma unroll
-    for (int r = 0; r < 6; ++r) {
-        const uint32_t f = fmix32(R ^ rk[r]) & mask;
+    for (int r = 0; r < ROUNDS; ++r) {
+        const uint32_t wl = (r & 1) ? b : a;          // width of the half being replaced
+        const uint32_t k = r < kRowWords ? w[r] : (w[r - kRowWords] ^ kKeyTweak);
+        const uint32_t f = fmix32(R ^ k) & ((1u << wl) - 1u);
         const uint32_t t = L ^ f;
         L = R; R = t;
     }
-    return (L << half) | R;
-}
-
-// P(j) for j < n.  The walk is bounded by the domain size (a permutation's
-// cycle through j returns to j within that many steps), so it always ends.
-__device__ __forceinline__ uint32_t permute(uint32_t j, const uint32_t rk[6], const FeistelDomain& d) {
-    uint32_t x = feistel6(j, rk, d.half, d.mask);
-    for (uint32_t it = 1; x >= d.n && it < d.size; ++it) x = feistel6(x, rk, d.half, d.mask);
-    return x < d.n ? x : 0u;
+    return (L << b) | R;
 }
 
 // Count rule: clamp(round_half_up(ppm * n / 1e6), 1, n).
