@@ -1,24 +1,34 @@
 // Sparse attention, tiled form: one workgroup per (kv_head g, 32 consecutive
-// query rows), one wavefront per query head of the GQA group.
+// query rows).
 //
 // When a row's unified set covers a sizeable share of its keys (a 70-seed
 // ensemble at 1% reaches ~50%), the sets of 32 neighbouring rows together
 // touch nearly every key block, so the work is a dense contraction under a
 // mask.  For every 64-key block the workgroup
-//   1. stages K[g, block] in LDS (row-major) and V[g, block] transposed, once
-//      for all 32 rows x G heads;
+//   1. stages K[g, block] and V[g, block] in LDS, row-major, once for all
+//      32 rows x G heads;
 //   2. turns each row's CSR entries that fall in the block into per-key tags
 //      in LDS (a window of 64 entries from the row's cursor suffices, the
 //      rows being ascending and unique);
-//   3. per wave (head h): S^T = K_blk Q_h^T on MFMA (32x32x16 bf16), masked by
-//      the tags, one online-softmax update per query over the block, and
-//      O^T += V_blk^T P^T on MFMA with P kept in registers.
-// Each lane owns one query column of S^T and of O^T, so the running max and
-// sum are per lane (plus one exchange with the lane 32 away): every index of a
-// row's set enters one normalisation (Pre-Fusion Unified Softmax; Methods,
-// "Hybrid Anchor and Pre-Fusion Unified Softmax").  In Structural mode the
-// block clique is the diagonal 64-key block: the dense local tile runs on
-// MFMA in the same softmax state as the sampled global keys.
+//   3. per wave: S^T = K_blk Q^T on MFMA, masked by the tags, one
+//      online-softmax update per query over the block, and O^T += V_blk^T P^T
+//      on MFMA with P kept in registers and V^T read from the row-major block
+//      with the LDS transpose read (ds_read_b64_tr_b16).
+// Every index of a row's set enters one normalisation (Pre-Fusion Unified
+// Softmax; Methods, "Hybrid Anchor and Pre-Fusion Unified Softmax").  In
+// Structural mode the block clique is the diagonal 64-key block: the dense
+// local tile runs on MFMA in the same softmax state as the sampled global keys.
+//
+// Two wave layouts, chosen by head dimension (measured on MI355X):
+//   * D = 128: k_attn_tile16 -- two waves per query head, 16 query rows each,
+//     MFMA 16x16x32.  A wave holds ~150 VGPRs, so the 2G waves of the
+//     workgroup sit three to a SIMD and the MFMA work of one wave overlaps the
+//     softmax of another; lane l holds query l % 16 in both products, so a
+//     query's running max and sum live in four lanes.
+//   * D = 64: k_attn_tile32 -- one wave per query head, all 32 rows, MFMA
+//     32x32x16; lane l holds query l % 32 and exchanges with lane l ^ 32.
+//     At D = 64 the 16-row layout doubles the LDS reads per MFMA flop and
+//     loses.
 #include "ris_device.h"
 #include "ris_internal.h"
 
@@ -40,10 +50,12 @@ __device__ __forceinline__ uint2 lds_read_tr16(const uint16_t* p) {
     return __builtin_bit_cast(uint2, v);
 }
 
-constexpr int kRows = kTileRows;   // query rows per tile (MFMA N)
 constexpr int kKeys = 64;   // keys per block
 
 __device__ __forceinline__ bf16x8_t as_bf16x8(uint4 v) {
+    return __builtin_bit_cast(bf16x8_t, v);
+}
+__device__ __forceinline__ bf16x8_t as_bf16x8(u32x4_t v) {
     return __builtin_bit_cast(bf16x8_t, v);
 }
 
@@ -72,14 +84,16 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
     return __builtin_bit_cast(uint32_t, __builtin_convertvector(f, bf16x2_t));
 }
 
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
 template <int D, int G>
-__global__ __launch_bounds__(64 * G) void k_attn_tile(AttnParams a, float c) {
+__global__ __launch_bounds__(64 * G) void k_attn_tile32(AttnParams a, float c) {
     constexpr int NT = 64 * G;
     constexpr int KS = D + 8;          // K row stride in LDS (bf16 elements)
     constexpr int VS = D + 16;         // V row stride: the 4 rows a 16-lane transpose read
                                        // touches start 8 banks apart
     constexpr int TS = kKeys + 4;      // tag row stride
-    constexpr int RPW = (kRows + G - 1) / G;
+    constexpr int RPW = (kTileRows + G - 1) / G;
     constexpr int KSTEPS = D / 16;
     constexpr int DT = D / 32;
     constexpr int KTASK = kKeys * (D / 8);          // 16-byte pieces of a K block
@@ -88,28 +102,28 @@ __global__ __launch_bounds__(64 * G) void k_attn_tile(AttnParams a, float c) {
     constexpr int VPT = (VTASK + NT - 1) / NT;
     __shared__ __align__(16) uint16_t Ks[kKeys * KS];
     __shared__ __align__(16) uint16_t Vs[kKeys * VS];
-    __shared__ __align__(16) uint16_t tags[kRows * TS];
-    __shared__ int64_t rstart_s[kRows];
-    __shared__ int32_t rlen_s[kRows];
+    __shared__ __align__(16) uint16_t tags[kTileRows * TS];
+    __shared__ int64_t rstart_s[kTileRows];
+    __shared__ int32_t rlen_s[kTileRows];
     __shared__ int32_t wcount[G];
     __shared__ int32_t kb_range[2];
 
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int hf = lane >> 5, n = lane & 31;
     const int64_t N = a.N;
-    const int64_t tiles = (N + kRows - 1) / kRows;
+    const int64_t tiles = (N + kTileRows - 1) / kTileRows;
     const int64_t bid = blockIdx.x;
     const int64_t tile = tiles - 1 - bid / a.Hkv;     // late (heavy) tiles first
     const int g = (int)(bid % a.Hkv);
-    const int64_t q0 = tile * kRows;
+    const int64_t q0 = tile * kTileRows;
     const int h = g * G + w;
     const uint16_t* Kg = static_cast<const uint16_t*>(a.K) + (int64_t)g * N * D;
     const uint16_t* Vg = static_cast<const uint16_t*>(a.V) + (int64_t)g * N * D;
     if (!tile_is_dense(a, g, q0)) return;   // a sparse tile belongs to the gather kernel
 
     // ---- per-row CSR extents, tags cleared
-    for (int i = tid; i < kRows * TS; i += NT) tags[i] = 0;
-    if (tid < kRows) {
+    for (int i = tid; i < kTileRows * TS; i += NT) tags[i] = 0;
+    if (tid < kTileRows) {
         const int64_t q = q0 + tid;
         int64_t s = 0, L = 0;
         if (q < N) {
@@ -123,7 +137,7 @@ __global__ __launch_bounds__(64 * G) void k_attn_tile(AttnParams a, float c) {
     // Key-block range touched by any row: first and last entries of each row.
     if (w == 0) {
         int lo = 0x7FFFFFFF, hi = -1;
-        if (lane < kRows && rlen_s[lane] > 0) {
+        if (lane < kTileRows && rlen_s[lane] > 0) {
             const int64_t nb = (N - 1) / kKeys;
             int64_t f = a.col_idx[rstart_s[lane]] / kKeys;
             int64_t l = a.col_idx[rstart_s[lane] + rlen_s[lane] - 1] / kKeys;
@@ -162,8 +176,8 @@ __global__ __launch_bounds__(64 * G) void k_attn_tile(AttnParams a, float c) {
 #pragma unroll
     for (int i = 0; i < RPW; ++i) {
         const int r = w + G * i;
-        rst[i] = r < kRows ? rstart_s[r] : 0;
-        rln[i] = r < kRows ? rlen_s[r] : 0;
+        rst[i] = r < kTileRows ? rstart_s[r] : 0;
+        rln[i] = r < kTileRows ? rlen_s[r] : 0;
         cur[i] = 0;
     }
     const int kb_lo = kb_range[0], kb_hi = kb_range[1];
@@ -227,7 +241,7 @@ __global__ __launch_bounds__(64 * G) void k_attn_tile(AttnParams a, float c) {
 #pragma unroll
         for (int i = 0; i < RPW; ++i) {
             const int r = w + G * i;
-            if (r < kRows) {
+            if (r < kTileRows) {
                 const int col = wreg[i];
                 const int k0i = kb * kKeys;
                 const bool inb = col >= k0i && col < k0i + kKeys && col < (int)N;
@@ -359,9 +373,274 @@ __global__ __launch_bounds__(64 * G) void k_attn_tile(AttnParams a, float c) {
 }
 
 template <int D, int G>
+__global__ __launch_bounds__(128 * G) void k_attn_tile16(AttnParams a, float c) {
+    constexpr int NW = 2 * G;                        // waves: (head, row half)
+    constexpr int NT = 64 * NW;
+    constexpr int KS = D + 16;          // K row stride in LDS (bf16 elements)
+    constexpr int VS = D + 16;         // V row stride: the 4 rows a 16-lane transpose read
+                                       // touches start 8 banks apart
+    constexpr int TS = kKeys + 4;      // tag row stride
+    constexpr int RPW = (kTileRows + NW - 1) / NW;       // tag rows per wave
+    constexpr int KSL = D / 32;                      // k-steps of the score product
+    constexpr int DT = D / 16;                       // 16-dim tiles of the output
+    constexpr int PIECES = kKeys * (D / 8);          // 16-byte pieces of a K (or V) block
+    constexpr int PPT = (PIECES + NT - 1) / NT;      // per thread
+    __shared__ __align__(16) uint16_t Ks[kKeys * KS];
+    __shared__ __align__(16) uint16_t Vs[kKeys * VS];
+    __shared__ __align__(16) uint16_t tags[kTileRows * TS];
+    __shared__ int64_t rstart_s[kTileRows];
+    __shared__ int32_t rlen_s[kTileRows];
+    __shared__ int32_t any_s[2];
+    __shared__ int32_t kb_range[2];
+
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int li = lane & 15, lg = lane >> 4;
+    const int hh = w >> 1, rh = w & 1;               // head of the group, row half
+    const int64_t N = a.N;
+    const int64_t tiles = (N + kTileRows - 1) / kTileRows;
+    const int64_t bid = blockIdx.x;
+    const int64_t tile = tiles - 1 - bid / a.Hkv;     // late (heavy) tiles first
+    const int g = (int)(bid % a.Hkv);
+    const int64_t q0 = tile * kTileRows;
+    const int h = g * G + hh;
+    const int qr = 16 * rh + li;                     // this lane's query row in the tile
+    const uint16_t* Kg = static_cast<const uint16_t*>(a.K) + (int64_t)g * N * D;
+    const uint16_t* Vg = static_cast<const uint16_t*>(a.V) + (int64_t)g * N * D;
+    if (!tile_is_dense(a, g, q0)) return;   // a sparse tile belongs to the gather kernel
+
+    // ---- per-row CSR extents, tags cleared
+    for (int i = tid; i < kTileRows * TS; i += NT) tags[i] = 0;
+    if (tid < 2) any_s[tid] = 0;
+    if (tid < kTileRows) {
+        const int64_t q = q0 + tid;
+        int64_t s = 0, L = 0;
+        if (q < N) {
+            s = a.row_ptr[g * N + q];
+            L = a.row_ptr[g * N + q + 1] - s;
+        }
+        rstart_s[tid] = s;
+        rlen_s[tid] = (int)L;
+    }
+    __syncthreads();
+    // Key-block range touched by any row: first and last entries of each row.
+    if (w == 0) {
+        int lo = 0x7FFFFFFF, hi = -1;
+        if (lane < kTileRows && rlen_s[lane] > 0) {
+            const int64_t nb = (N - 1) / kKeys;
+            int64_t f = a.col_idx[rstart_s[lane]] / kKeys;
+            int64_t l = a.col_idx[rstart_s[lane] + rlen_s[lane] - 1] / kKeys;
+            f = f < 0 ? 0 : (f > nb ? nb : f);
+            l = l < 0 ? 0 : (l > nb ? nb : l);
+            lo = (int)f;
+            hi = (int)l;
+        }
+        for (int off = 32; off > 0; off >>= 1) {
+            lo = min(lo, __shfl_xor(lo, off));
+            hi = max(hi, __shfl_xor(hi, off));
+        }
+        if (lane == 0) { kb_range[0] = lo; kb_range[1] = hi; }
+    }
+
+    // ---- this lane's query row of Q_h as the B operand: dims 32 ks + 8 (l/16) ..
+    u32x4_t qf[KSL];
+    {
+        const int64_t q = q0 + qr;
+        const uint16_t* Qrow = static_cast<const uint16_t*>(a.Q) + ((int64_t)h * N + (q < N ? q : 0)) * D;
+        const u32x4_t zero = {0u, 0u, 0u, 0u};
+#pragma unroll
+        for (int ks = 0; ks < KSL; ++ks) {
+            const u32x4_t v = *reinterpret_cast<const u32x4_t*>(Qrow + 32 * ks + 8 * lg);
+            qf[ks] = q < N ? v : zero;
+        }
+    }
+    float m_run = -INFINITY, l_run = 0.f;
+    f32x4_t o[DT];
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) o[dt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    __syncthreads();
+
+    // Rows this wave turns into tags: r = w + NW*i.
+    int64_t rst[RPW];
+    int rln[RPW], cur[RPW];
+#pragma unroll
+    for (int i = 0; i < RPW; ++i) {
+        const int r = w + NW * i;
+        rst[i] = r < kTileRows ? rstart_s[r] : 0;
+        rln[i] = r < kTileRows ? rlen_s[r] : 0;
+        cur[i] = 0;
+    }
+    const int kb_lo = kb_range[0], kb_hi = kb_range[1];
+
+    // ---- register staging of one block (K and V pieces, CSR windows)
+    u32x4_t kreg[PPT], vreg[PPT];
+    int wreg[RPW];
+    auto load_kv = [&](int kb) {
+        const int k0 = kb * kKeys;
+#pragma unroll
+        for (int u = 0; u < PPT; ++u) {
+            const int e = tid + u * NT;
+            const int key = e / (D / 8), ch = e % (D / 8);
+            const int64_t j = min(k0 + key, (int)N - 1);   // rows past N are masked out
+            if (PIECES % NT == 0 || e < PIECES) {
+                kreg[u] = *reinterpret_cast<const u32x4_t*>(Kg + j * D + ch * 8);
+                vreg[u] = *reinterpret_cast<const u32x4_t*>(Vg + j * D + ch * 8);
+            }
+        }
+    };
+    auto load_windows = [&]() {
+#pragma unroll
+        for (int i = 0; i < RPW; ++i)
+            wreg[i] = lane < rln[i] - cur[i] ? a.col_idx[rst[i] + cur[i] + lane] : -1;
+    };
+
+    if (kb_lo <= kb_hi) {
+        load_kv(kb_lo);
+        load_windows();
+    }
+    for (int kb = kb_lo; kb <= kb_hi; ++kb) {
+        const int64_t k0 = (int64_t)kb * kKeys;
+        // ---- registers -> LDS, both row-major
+#pragma unroll
+        for (int u = 0; u < PPT; ++u) {
+            const int e = tid + u * NT;
+            if (PIECES % NT == 0 || e < PIECES) {
+                const int key = e / (D / 8), ch = e % (D / 8);
+                *reinterpret_cast<u32x4_t*>(&Ks[key * KS + ch * 8]) = kreg[u];   // rows past N: masked
+                u32x4_t v = vreg[u];
+                if (k0 + key >= N) v = u32x4_t{0u, 0u, 0u, 0u};   // V rows past N read as zeros
+                *reinterpret_cast<u32x4_t*>(&Vs[key * VS + ch * 8]) = v;
+            }
+        }
+        // ---- the next block's K/V loads fly from here until its staging
+        if (kb < kb_hi) load_kv(kb + 1);
+        // ---- tags: keys of this block present in each row's set
+        const uint16_t tag = (uint16_t)(kb + 1);
+        int my_cnt = 0;
+#pragma unroll
+        for (int i = 0; i < RPW; ++i) {
+            const int r = w + NW * i;
+            if (r < kTileRows) {
+                const int col = wreg[i];
+                const int k0i = kb * kKeys;
+                const bool inb = col >= k0i && col < k0i + kKeys && col < (int)N;
+                const uint64_t bal = __ballot(inb);
+                if (inb) tags[r * TS + (col - k0i)] = tag;
+                const int cnt = __popcll(bal);
+                cur[i] += cnt;
+                my_cnt += cnt;
+            }
+        }
+        if (lane == 0 && my_cnt) any_s[kb & 1] = 1;
+        __syncthreads();
+        // ---- next block's CSR windows (cursors are now past this block)
+        if (kb < kb_hi) load_windows();
+        const int any = any_s[kb & 1];
+        if (tid == 0) any_s[(kb + 1) & 1] = 0;
+
+        if (any) {
+            // ---- S^T[key, query] = K_blk Q_h^T; st[kt][i] is key 16 kt + 4 (l/16) + i
+            f32x4_t st[4];
+#pragma unroll
+            for (int kt = 0; kt < 4; ++kt) {
+                st[kt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int ks = 0; ks < KSL; ++ks) {
+                    const u32x4_t av = *reinterpret_cast<const u32x4_t*>(&Ks[(16 * kt + li) * KS + 32 * ks + 8 * lg]);
+                    st[kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(av), as_bf16x8(qf[ks]), st[kt],
+                                                                      0, 0, 0);
+                }
+            }
+            // ---- mask, one online-softmax step for this lane's query
+            float mx = -INFINITY;
+#pragma unroll
+            for (int kt = 0; kt < 4; ++kt) {
+                const uint2 tg = *reinterpret_cast<const uint2*>(&tags[qr * TS + 16 * kt + 4 * lg]);
+                const uint32_t tv[4] = {tg.x & 0xFFFFu, tg.x >> 16, tg.y & 0xFFFFu, tg.y >> 16};
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const float s = tv[i] == tag ? st[kt][i] : -INFINITY;
+                    st[kt][i] = s;
+                    mx = fmaxf(mx, s);
+                }
+            }
+            mx = fmaxf(mx, __shfl_xor(mx, 16));
+            mx = fmaxf(mx, __shfl_xor(mx, 32));
+            const float m_new = fmaxf(m_run, mx);
+            const float m_use = m_new == -INFINITY ? 0.f : m_new;
+            const float mc = m_use * c;
+            float rs = 0.f;
+#pragma unroll
+            for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const float p = __builtin_amdgcn_exp2f(fmaf(st[kt][i], c, -mc));
+                    st[kt][i] = p;
+                    rs += p;
+                }
+            if (__ballot(m_new != m_run) != 0ull) {      // some query's max moved: rescale
+                const float corr = __builtin_amdgcn_exp2f(fmaf(m_run, c, -mc));
+                l_run *= corr;
+#pragma unroll
+                for (int dt = 0; dt < DT; ++dt) o[dt] *= corr;
+            }
+            l_run += rs;
+            m_run = m_new;
+            // ---- P^T as the B operand: 32-key step u holds keys 32u + 4 (l/16) + i
+            // (slots 0..3) and 32u + 16 + 4 (l/16) + i (slots 4..7)
+            u32x4_t pb[2];
+#pragma unroll
+            for (int u = 0; u < 2; ++u)
+                pb[u] = u32x4_t{pack_bf16x2(st[2 * u][0], st[2 * u][1]), pack_bf16x2(st[2 * u][2], st[2 * u][3]),
+                                pack_bf16x2(st[2 * u + 1][0], st[2 * u + 1][1]),
+                                pack_bf16x2(st[2 * u + 1][2], st[2 * u + 1][3])};
+            // ---- O^T[d, query] += V_blk^T P^T: lane l addresses key row l/4
+            // (then 16 + l/4) of the step at dims 16 dt + 4 (l%4)
+#pragma unroll
+            for (int u = 0; u < 2; ++u) {
+                const uint16_t* v_lo = &Vs[(32 * u + (lane >> 2)) * VS + 4 * (lane & 3)];
+#pragma unroll
+                for (int dt = 0; dt < DT; ++dt) {
+                    const uint2 lo = lds_read_tr16(v_lo + 16 * dt);
+                    const uint2 hi = lds_read_tr16(v_lo + 16 * VS + 16 * dt);
+                    const u32x4_t av = {lo.x, lo.y, hi.x, hi.y};
+                    o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(av), as_bf16x8(pb[u]), o[dt], 0, 0, 0);
+                }
+            }
+        }
+        __syncthreads();
+    }
+
+    // ---- normalise and store: o[dt][i] is dim 16 dt + 4 (l/16) + i of the query
+    l_run += __shfl_xor(l_run, 16);
+    l_run += __shfl_xor(l_run, 32);
+    const int64_t q = q0 + qr;
+    if (q < N) {
+        const float inv = l_run > 0.f ? 1.0f / l_run : 0.f;
+        const int64_t base = ((int64_t)h * N + q) * D;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) {
+            const int d = 16 * dt + 4 * lg;
+            const float v0 = o[dt][0] * inv, v1 = o[dt][1] * inv;
+            const float v2 = o[dt][2] * inv, v3 = o[dt][3] * inv;
+            if (a.out_bf16) {
+                *reinterpret_cast<uint2*>(static_cast<uint16_t*>(a.out) + base + d) =
+                    make_uint2(pack_bf16x2(v0, v1), pack_bf16x2(v2, v3));
+            } else {
+                *reinterpret_cast<float4*>(static_cast<float*>(a.out) + base + d) =
+                    make_float4(v0, v1, v2, v3);
+            }
+        }
+    }
+}
+
+template <int D, int G>
 hipError_t launch_d_g(const AttnParams& a, float c, hipStream_t st) {
-    const int64_t tiles = (a.N + kRows - 1) / kRows;
-    hipLaunchKernelGGL((k_attn_tile<D, G>), dim3((unsigned)(tiles * a.Hkv)), dim3(64 * G), 0, st, a, c);
+    const int64_t tiles = (a.N + kTileRows - 1) / kTileRows;
+    const dim3 grid((unsigned)(tiles * a.Hkv));
+    if constexpr (D == 128)
+        hipLaunchKernelGGL((k_attn_tile16<D, G>), grid, dim3(128 * G), 0, st, a, c);
+    else
+        hipLaunchKernelGGL((k_attn_tile32<D, G>), grid, dim3(64 * G), 0, st, a, c);
     return hipGetLastError();
 }
 
