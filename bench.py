@@ -378,7 +378,7 @@ def main():
                    "density": w.density_ppm / 1e6, "seeds": w.n_seeds, "block": w.block,
                    "window": w.window, "anchor": w.anchor,
                    "rope": ["none", "plain", "linear", "yarn"][w.rope + 1],
-                   "layers": f"0..{len(layers) - 1}" if len(layers) > 1 else args.layer},
+                   **({"layers": f"0..{len(layers) - 1}"} if len(layers) > 1 else {"layer": args.layer})},
         "ms_per_layer_attn": g["ms_attn"] / len(layers),
         "ms_attn": g["ms_attn"],
         "ms_geometry": g["ms_mask"],
@@ -389,7 +389,8 @@ def main():
         "hbm_gbs_attn": achieved,
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
-                     "kernel": "k_attn_tile" if tiled else "k_attn_gather",
+                     "kernel": (f"k_attn_tile{16 if w.D == 128 else 32}<{w.D}, {G}>" if tiled
+                                else f"k_attn_gather<{w.D}>"),
                      "bytes_per_kv_pair": KV_PAIR_BYTES[w.D]},
         # The tiled kernel reads each K/V block once per 32 rows, so its real
         # bound is matrix/vector work: the method's flops (4 D G per kv-pair:
