@@ -271,11 +271,35 @@ int ris_decode_attn(const void* Q, const void* K, const void* V, const int64_t* 
                     void* workspace, int64_t workspace_bytes, const ris_decode_desc* desc,
                     void* stream);
 
+/* ------------------------------------------------------------------------ */
+/* Host-model layers for a model-level prefill                               */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * The host models' normalisation, not part of the method (the paper replaces
+ * only the attention kernel and leaves weights and every other component
+ * untouched; Methods, opening of "The RIS Implementation").  Row-major [rows, cols] tensors of element type dtype
+ * (ris_dtype); weight has cols entries.  With residual != NULL:
+ * r = x + residual, residual <- r (rounded to dtype), out = rmsnorm(r);
+ * otherwise out = rmsnorm(x).  rmsnorm(r) = r / sqrt(mean(r^2) + eps) * weight,
+ * in float32 with one rounding at the store.  out may alias x.
+ */
+int ris_rmsnorm(const void* x, void* residual, const void* weight, void* out, int64_t rows,
+                int64_t cols, float eps, int32_t dtype, void* stream);
+
+/*
+ * The SwiGLU activation of the host models' MLP: gate_up is [rows, 2*inter]
+ * (gate in the first inter columns, up in the rest), out is [rows, inter] with
+ * out = silu(gate) * up, silu(g) = g / (1 + exp(-g)), in float32.
+ */
+int ris_swiglu(const void* gate_up, void* out, int64_t rows, int64_t inter, int32_t dtype, void* stream);
+
 /* Human-readable name of a ris_status (static string, never NULL). */
 const char* ris_status_string(int status);
 
 /* Library ABI version: (major << 16) | minor.  2.0 added window and anchor to
- * ris_mask_desc; 2.1 added the row-range build and the decode step. */
+ * ris_mask_desc; 2.1 added the row-range build and the decode step; 2.2 the
+ * host-model layers (RMSNorm, SwiGLU). */
 int ris_version(void);
 
 #ifdef __cplusplus

@@ -22,9 +22,11 @@ Modules, in the order the method runs:
                   "Hybrid Anchor and Pre-Fusion Unified Softmax") and PV.
 * ``decode``   -- the Hybrid-Anchor generation step: frozen stochastic anchor
                   plus sliding local window, merged, one softmax (same passage).
+* ``model``    -- a LLaMA / Qwen2 decoder stack around the RIS attention
+                  (model-level prefill; Methods, "The RIS Implementation").
 
 Every floating-point step runs in float64.  Readings of the paper where it is
 silent or ambiguous are listed in the module that takes them.
 """
 
-from . import philox, prp, geometry, rope, attention, decode  # noqa: F401
+from . import philox, prp, geometry, rope, attention, decode, model  # noqa: F401

@@ -98,7 +98,7 @@ constexpr float kAutoDensity = 0.06f;
 
 extern "C" {
 
-int ris_version(void) { return (2 << 16) | 1; }
+int ris_version(void) { return (2 << 16) | 2; }
 
 const char* ris_status_string(int status) {
     switch (status) {
@@ -294,6 +294,24 @@ int64_t decode_workspace(const ris_decode_desc& d) {
 }  // namespace
 
 extern "C" {
+
+int ris_rmsnorm(const void* x, void* residual, const void* weight, void* out, int64_t rows,
+                int64_t cols, float eps, int32_t dtype, void* stream) {
+    if (!x || !weight || !out) return RIS_E_ARG;
+    if (dtype != RIS_F32 && dtype != RIS_BF16) return RIS_E_DTYPE;
+    if (rows < 1 || rows > 0x7FFFFFFFll || cols < 1 || cols > (1 << 20)) return RIS_E_ARG;
+    if (!(eps > 0.0f) || !isfinite(eps)) return RIS_E_ARG;
+    return hip_status(ris::launch_rmsnorm(x, residual, weight, out, rows, cols, eps, dtype == RIS_BF16,
+                                          static_cast<hipStream_t>(stream)));
+}
+
+int ris_swiglu(const void* gate_up, void* out, int64_t rows, int64_t inter, int32_t dtype, void* stream) {
+    if (!gate_up || !out) return RIS_E_ARG;
+    if (dtype != RIS_F32 && dtype != RIS_BF16) return RIS_E_DTYPE;
+    if (rows < 1 || inter < 1 || rows > (1ll << 40) / inter) return RIS_E_ARG;
+    return hip_status(ris::launch_swiglu(gate_up, out, rows, inter, dtype == RIS_BF16,
+                                         static_cast<hipStream_t>(stream)));
+}
 
 int64_t ris_decode_workspace_bytes(const ris_decode_desc* desc) {
     const int st = validate_decode(desc);

@@ -95,4 +95,9 @@ struct DecodeParams {
 };
 hipError_t launch_decode(const DecodeParams& p, hipStream_t st);
 
+// Host-model layers around the attention (model-level prefill).
+hipError_t launch_rmsnorm(const void* x, void* residual, const void* w, void* out, int64_t rows,
+                          int64_t cols, float eps, int bf16, hipStream_t st);
+hipError_t launch_swiglu(const void* gu, void* out, int64_t rows, int64_t inter, int bf16, hipStream_t st);
+
 }  // namespace ris

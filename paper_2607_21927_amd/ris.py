@@ -72,6 +72,10 @@ def lib():
         L.ris_mask_build_rows.restype = ctypes.c_int
         L.ris_mask_rows_nnz_bound.argtypes = [ctypes.POINTER(MaskDesc), i64, i64]
         L.ris_mask_rows_nnz_bound.restype = i64
+        L.ris_rmsnorm.argtypes = [vp, vp, vp, vp, i64, i64, ctypes.c_float, i32, vp]
+        L.ris_rmsnorm.restype = ctypes.c_int
+        L.ris_swiglu.argtypes = [vp, vp, i64, i64, i32, vp]
+        L.ris_swiglu.restype = ctypes.c_int
         L.ris_decode_workspace_bytes.argtypes = [ctypes.POINTER(DecodeDesc)]
         L.ris_decode_workspace_bytes.restype = i64
         L.ris_decode_attn.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, i64,
@@ -91,7 +95,8 @@ def lib():
 
 EXPORTS = ("ris_mask_build", "ris_mask_nnz_bound", "ris_mask_build_rows",
            "ris_mask_rows_nnz_bound", "ris_rope", "ris_sparse_attn",
-           "ris_decode_workspace_bytes", "ris_decode_attn", "ris_status_string", "ris_version")
+           "ris_decode_workspace_bytes", "ris_decode_attn", "ris_rmsnorm", "ris_swiglu",
+           "ris_status_string", "ris_version")
 
 
 def status_string(status):
@@ -217,6 +222,30 @@ def decode_attn(Q, K, V, pos, anchor_ptr, anchor_idx, out, workspace, desc, stre
     _check(lib().ris_decode_attn(_ptr(Q), _ptr(K), _ptr(V), _ptr(pos), _ptr(anchor_ptr),
                                  _ptr(anchor_idx), _ptr(out), _ptr(workspace), nbytes,
                                  ctypes.byref(desc), _stream(stream)), "ris_decode_attn")
+    return out
+
+
+def rmsnorm(x, weight, out, eps, residual=None, stream=None):
+    """ris_rmsnorm over the last dimension of x (rows = everything else)."""
+    _need_device(x, weight, out, residual)
+    cols = x.shape[-1]
+    if weight.numel() != cols or out.shape != x.shape or (residual is not None and residual.shape != x.shape):
+        raise ValueError("shapes: weight [cols], out and residual like x")
+    if not (x.dtype == weight.dtype == out.dtype) or (residual is not None and residual.dtype != x.dtype):
+        raise TypeError("x, weight, out (and residual) must share a dtype")
+    _check(lib().ris_rmsnorm(_ptr(x), _ptr(residual), _ptr(weight), _ptr(out), x.numel() // cols, cols,
+                             eps, _dtype_code(x), _stream(stream)), "ris_rmsnorm")
+    return out
+
+
+def swiglu(gate_up, out, stream=None):
+    """ris_swiglu: out [rows, I] from gate_up [rows, 2I]."""
+    _need_device(gate_up, out)
+    inter = out.shape[-1]
+    if gate_up.shape[-1] != 2 * inter or gate_up.numel() != 2 * out.numel() or gate_up.dtype != out.dtype:
+        raise ValueError("gate_up must be [rows, 2*inter] of out's dtype")
+    _check(lib().ris_swiglu(_ptr(gate_up), _ptr(out), out.numel() // inter, inter, _dtype_code(out),
+                            _stream(stream)), "ris_swiglu")
     return out
 
 

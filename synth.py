@@ -143,3 +143,72 @@ def decode_inputs(B, Hq, Hkv, max_len, D, seed=0):
     K = rng.standard_normal((B, Hkv, max_len, D), dtype=np.float32)
     V = rng.standard_normal((B, Hkv, max_len, D), dtype=np.float32)
     return Q, K, V
+
+
+# ---------------------------------------------------------------------------
+# Host-model shapes for a model-level prefill with random weights.
+# ---------------------------------------------------------------------------
+@dataclass(frozen=True)
+class ModelConfig:
+    name: str
+    hidden: int
+    heads: int
+    kv_heads: int
+    head_dim: int
+    inter: int                 # MLP intermediate size
+    layers: int
+    eps: float                 # RMSNorm epsilon
+    rope_base: float
+    qkv_bias: bool             # Qwen2 has q/k/v biases, LLaMA does not
+    vocab: int
+    native_len: int            # positional limit the model was trained to
+
+    def with_layers(self, n):
+        return replace(self, layers=n)
+
+
+MODELS = {
+    "qwen2_1.5b": ModelConfig("qwen2_1.5b", 1536, 12, 2, 128, 8960, 28, 1e-6, 1e6, True, 151936, 32768),
+    "tinyllama_1.1b": ModelConfig("tinyllama_1.1b", 2048, 32, 4, 64, 5632, 22, 1e-5, 1e4, False, 32000,
+                                  2048),
+    # small stand-ins with the same layer structure, for parity tests
+    "tiny_qwen2": ModelConfig("tiny_qwen2", 256, 4, 2, 64, 512, 2, 1e-6, 1e6, True, 500, 128),
+    "tiny_llama": ModelConfig("tiny_llama", 384, 6, 2, 64, 640, 2, 1e-5, 1e4, False, 500, 128),
+}
+
+
+def model_weights(cfg, seed=0):
+    """Random weights of a decoder stack, float32, from
+    ``numpy.random.default_rng(seed)`` in a fixed order: embedding, then per
+    layer q, k, v (+ biases), o, gate, up, down and the two norm weights, then
+    the final norm.  Linear weights and embeddings ~ N(0, 0.02^2), biases
+    ~ N(0, 0.02^2), norm weights ~ 1 + N(0, 0.1^2).  Linear weights are stored
+    [out_features, in_features]."""
+    rng = np.random.default_rng(seed)
+    f = np.float32
+
+    def lin(o, i):
+        return (0.02 * rng.standard_normal((o, i))).astype(f)
+
+    W = {"embed": (0.02 * rng.standard_normal((cfg.vocab, cfg.hidden))).astype(f), "layers": []}
+    qd, kd = cfg.heads * cfg.head_dim, cfg.kv_heads * cfg.head_dim
+    for _ in range(cfg.layers):
+        L = {"q": lin(qd, cfg.hidden), "k": lin(kd, cfg.hidden), "v": lin(kd, cfg.hidden)}
+        if cfg.qkv_bias:
+            L["bq"] = (0.02 * rng.standard_normal(qd)).astype(f)
+            L["bk"] = (0.02 * rng.standard_normal(kd)).astype(f)
+            L["bv"] = (0.02 * rng.standard_normal(kd)).astype(f)
+        L["o"] = lin(cfg.hidden, qd)
+        L["gate"] = lin(cfg.inter, cfg.hidden)
+        L["up"] = lin(cfg.inter, cfg.hidden)
+        L["down"] = lin(cfg.hidden, cfg.inter)
+        L["ln1"] = (1 + 0.1 * rng.standard_normal(cfg.hidden)).astype(f)
+        L["ln2"] = (1 + 0.1 * rng.standard_normal(cfg.hidden)).astype(f)
+        W["layers"].append(L)
+    W["norm"] = (1 + 0.1 * rng.standard_normal(cfg.hidden)).astype(f)
+    return W
+
+
+def tokens(n, vocab, seed=0):
+    """n token ids uniform in [0, vocab) from ``default_rng(seed)``."""
+    return np.random.default_rng(seed).integers(0, vocab, size=n)

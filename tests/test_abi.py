@@ -34,8 +34,8 @@ def test_header_declares_the_boundary():
     names = declared_functions()
     assert names == sorted(["ris_mask_build", "ris_mask_nnz_bound", "ris_mask_build_rows",
                             "ris_mask_rows_nnz_bound", "ris_rope", "ris_sparse_attn",
-                            "ris_decode_workspace_bytes", "ris_decode_attn",
-                            "ris_status_string", "ris_version"])
+                            "ris_decode_workspace_bytes", "ris_decode_attn", "ris_rmsnorm",
+                            "ris_swiglu", "ris_status_string", "ris_version"])
 
 
 def test_library_exports_every_declared_symbol(ris):
@@ -52,7 +52,7 @@ def test_status_strings_and_version(ris):
     for code in (0, -1, -2, -3, -4, -5, -6):
         assert ris.status_string(code).startswith("RIS_")
     assert ris.status_string(123) == "unknown ris_status"
-    assert ris.version() >> 16 == 2
+    assert ris.version() >> 16 == 2 and ris.version() & 0xFFFF >= 2
 
 
 def _mask(ris, **kw):
@@ -194,3 +194,15 @@ def test_decode_workspace_size_and_capacity_error(ris):
     need = ris.decode_workspace_bytes(d)
     assert L.ris_decode_attn(f, f, f, f, f, f, f, f, need - 1, ctypes.byref(d), None) == -4
     assert L.ris_decode_attn(f, f, f, f, f, None, f, f, need, ctypes.byref(d), None) == -1
+
+
+def test_host_layer_validation(ris):
+    L = ris.lib()
+    f = ctypes.c_void_p(0x1000)
+    assert L.ris_rmsnorm(None, None, f, f, 4, 8, 1e-6, 1, None) == -1
+    assert L.ris_rmsnorm(f, None, f, f, 4, 8, 1e-6, 5, None) == -3
+    assert L.ris_rmsnorm(f, None, f, f, 0, 8, 1e-6, 1, None) == -1
+    assert L.ris_rmsnorm(f, None, f, f, 4, 8, 0.0, 1, None) == -1
+    assert L.ris_swiglu(f, None, 4, 8, 1, None) == -1
+    assert L.ris_swiglu(f, f, 4, 0, 1, None) == -1
+    assert L.ris_swiglu(f, f, 4, 8, 2, None) == -3
