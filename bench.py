@@ -24,7 +24,8 @@ import numpy as np
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
-from synth import ROPE_NONE, STRUCTURAL, WORKLOADS, gaussian_qkv, needle_plan, plant_needles  # noqa: E402
+from synth import (ROPE_LINEAR, ROPE_NONE, ROPE_YARN, STRUCTURAL, WORKLOADS, gaussian_qkv,  # noqa: E402
+                   needle_plan, plant_needles)
 
 HBM_PEAK_GBS = 8000.0
 MFMA_BF16_PEAK_TFS = 2500.0          # dense bf16 matrix peak of MI355X
@@ -313,6 +314,107 @@ def run_decode_bench(w, B, steps, warmup, cpu):
     }
 
 
+# ---------------------------------------------------------------------------
+# Model-level prefill (random weights): --model
+# ---------------------------------------------------------------------------
+class PhaseTimer:
+    """HIP events between phase marks; time from one mark to the next is
+    charged to the later mark's name."""
+
+    def __init__(self, torch):
+        self.torch = torch
+        self.marks = []
+
+    def mark(self, name):
+        e = self.torch.cuda.Event(enable_timing=True)
+        e.record()
+        self.marks.append((name, e))
+
+    def totals(self):
+        self.torch.cuda.synchronize()
+        out = {}
+        for (_, a), (name, b) in zip(self.marks, self.marks[1:]):
+            out[name] = out.get(name, 0.0) + a.elapsed_time(b)
+        return out
+
+
+MODEL_WORKLOAD = {"qwen2_1.5b": "qwen2_64k_stochastic_yarn", "tinyllama_1.1b": "tinyllama_64k_structural"}
+
+
+def run_model_bench(name, layers, steps, warmup):
+    import torch
+    from paper_2607_21927_amd import ris
+    from paper_2607_21927_amd.model import PrefillModel
+    from synth import MODELS
+    cfg = MODELS[name] if not layers else MODELS[name].with_layers(layers)
+    w = WORKLOADS[MODEL_WORKLOAD[name]]
+    dev = torch.device("cuda:0")
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(0)
+
+    def rnd(*shape, std=0.02, mean=0.0):
+        return (torch.randn(*shape, generator=gen, device=dev) * std + mean).to(torch.bfloat16)
+
+    qd, kd = cfg.heads * cfg.head_dim, cfg.kv_heads * cfg.head_dim
+    W = {"embed": rnd(cfg.vocab, cfg.hidden), "layers": [], "norm": rnd(cfg.hidden, std=0.1, mean=1.0)}
+    for _ in range(cfg.layers):
+        L = {"q": rnd(qd, cfg.hidden), "k": rnd(kd, cfg.hidden), "v": rnd(kd, cfg.hidden),
+             "o": rnd(cfg.hidden, qd), "gate": rnd(cfg.inter, cfg.hidden), "up": rnd(cfg.inter, cfg.hidden),
+             "down": rnd(cfg.hidden, cfg.inter), "ln1": rnd(cfg.hidden, std=0.1, mean=1.0),
+             "ln2": rnd(cfg.hidden, std=0.1, mean=1.0)}
+        if cfg.qkv_bias:
+            L.update(bq=rnd(qd), bk=rnd(kd), bv=rnd(kd))
+        W["layers"].append(L)
+    model = PrefillModel(cfg, W, dev, torch.bfloat16)
+    del W
+    N = w.N
+    ids = torch.randint(0, cfg.vocab, (N,), generator=gen, device=dev)
+    mask = dict(mode=w.mode, density_ppm=w.density_ppm, n_seeds=w.n_seeds, block=w.block)
+    runs = {}
+    for kind, label in [(ROPE_YARN, "yarn"), (ROPE_LINEAR, "linear")]:
+        rd = ris.rope_desc(kind, cfg.rope_base, orig_max_pos=cfg.native_len)
+        for _ in range(warmup):
+            model.prefill(ids, mask, rd)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(steps):
+            out = model.prefill(ids, mask, rd)
+        e1.record()
+        torch.cuda.synchronize()
+        runs[label] = {"ms": e0.elapsed_time(e1) / steps, "out": out.float()}
+    timer = PhaseTimer(torch)
+    timer.mark("start")
+    model.prefill(ids, mask, ris.rope_desc(ROPE_YARN, cfg.rope_base, orig_max_pos=cfg.native_len),
+                  timers=timer)
+    timer.mark("proj")
+    phases = timer.totals()
+    a, b = runs["yarn"]["out"], runs["linear"]["out"]
+    rel = float((a - b).norm() / a.norm())
+    ms = runs["yarn"]["ms"]
+    return {
+        "metric": "model-level prefill tokens/s (random-weight decoder stack, RIS attention)",
+        "value": N / (ms * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic: random weights and token ids (torch.randn / randint, seed 0)",
+        "config": {"workload": f"{name}_prefill_{N}", "layers": cfg.layers, "hidden": cfg.hidden,
+                   "geometry": MODEL_WORKLOAD[name], "rope": "yarn (factor N / native)"},
+        "phase_ms_per_prefill": {k: v for k, v in phases.items()},
+        "ablation_rope": {"yarn_ms": runs["yarn"]["ms"], "linear_ms": runs["linear"]["ms"],
+                          "relative_l2_difference_of_final_states": rel},
+        "roofline": None,
+        "cpu_baseline": None,
+    }
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -329,11 +431,17 @@ def main():
     ap.add_argument("--decode", action="store_true",
                     help="time the Hybrid-Anchor decode step instead of the prefill layer")
     ap.add_argument("--batch", type=int, default=32, help="sequences per decode step")
+    ap.add_argument("--model", choices=sorted(MODEL_WORKLOAD),
+                    help="time a model-level prefill of the named random-weight stack")
+    ap.add_argument("--model-layers", type=int, default=0, help="layers of the stack (0 = all)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: the hot path needs no cross-GPU exchange and this "
               "build has no multi-GPU launch (run with --gpus 1).", file=sys.stderr)
         sys.exit(2)
+    if args.model:
+        print(json.dumps(run_model_bench(args.model, args.model_layers, args.steps, args.warmup)))
+        return
     if args.decode:
         wl = args.workload if args.workload != "qwen2_64k_stochastic_yarn" else "qwen2_64k_full_geometry"
         print(json.dumps(run_decode_bench(WORKLOADS[wl], args.batch, args.steps, args.warmup,

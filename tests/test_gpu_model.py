@@ -1,0 +1,92 @@
+"""GPU model-level prefill (PrefillModel over ris_*) vs the oracle stack.
+
+float32 end to end: every kernel accumulates in float32, the GEMMs are
+float32 library GEMMs (contraction length K <= 640 here), so a layer's
+outputs move by at most about K float32 ulps (640 x 2^-24 ~ 4e-5 relative)
+of their inputs, and the final RMSNorm'd states (values of order 1, below 5)
+stay within 5e-5 of the float64 oracle.
+bfloat16: activations are rounded to bf16 between every step (relative
+2^-9 each, about 20 roundings per layer), so the bound is looser: 0.15
+absolute on order-1 outputs over two layers, plus agreement in direction
+(cosine > 0.999).
+"""
+from dataclasses import replace
+
+import numpy as np
+import pytest
+
+from gpu_common import need_gpu, say, torch
+from oracle import geometry as o_geo
+from oracle import model as o_model
+from oracle import rope as o_rope
+from synth import MODELS, model_weights, tokens
+
+pytestmark = pytest.mark.gpu
+
+CASES = [
+    # model, N, mode, ppm, seeds, block, window, anchor, rope kind, factor
+    ("tiny_qwen2", 300, 0, 50_000, 3, 0, 32, 2, o_rope.YARN, 0.0),
+    ("tiny_qwen2", 300, 0, 50_000, 3, 0, 32, 2, o_rope.LINEAR, 0.0),
+    ("tiny_llama", 257, 1, 100_000, 4, 16, 0, 0, o_rope.YARN, 4.0),
+    ("tiny_llama", 200, 0, 10**6, 1, 0, 0, 0, o_rope.PLAIN, 0.0),      # dense causal
+]
+
+
+def run(case, dtype):
+    ris = need_gpu()
+    from paper_2607_21927_amd.model import PrefillModel
+    name, N, mode, ppm, S, block, window, anchor, kind, factor = case
+    cfg = MODELS[name]
+    W = model_weights(cfg, seed=7)
+    ids = tokens(N, cfg.vocab, seed=8)
+    spec = o_geo.MaskSpec(mode=mode, density_ppm=ppm, seed=0, n_seeds=S, layer=0, N=N,
+                          heads=cfg.kv_heads, block=block, window=window, anchor=anchor)
+    want = o_model.prefill(ids, W, cfg, spec, kind, factor)
+    model = PrefillModel(cfg, W, "cuda", dtype)
+    rd = ris.rope_desc(kind, cfg.rope_base, orig_max_pos=cfg.native_len, factor=factor)
+    mask = dict(mode=mode, density_ppm=ppm, n_seeds=S, block=block, window=window, anchor=anchor)
+    got = model.prefill(torch.tensor(ids, device="cuda"), mask, rd).float().cpu().numpy()
+    return got, want
+
+
+@pytest.mark.parametrize("case", CASES)
+def test_model_prefill_float32_matches_oracle(case):
+    say(f"model parity f32 {case}")
+    got, want = run(case, torch.float32)
+    err = float(np.abs(got - want).max())
+    say(f"  max err {err:.3e} (max |want| {np.abs(want).max():.2f})")
+    assert err <= 5e-5
+
+
+@pytest.mark.parametrize("case", CASES[:1] + CASES[2:3])
+def test_model_prefill_bf16_close_to_oracle(case):
+    got, want = run(case, torch.bfloat16)
+    err = float(np.abs(got - want).max())
+    cos = float((got * want).sum() / (np.linalg.norm(got) * np.linalg.norm(want)))
+    say(f"  bf16 max err {err:.3e}, cosine {cos:.6f}")
+    assert np.isfinite(got).all() and err <= 0.15 and cos > 0.999
+
+
+def test_host_layers_match_closed_forms():
+    """ris_rmsnorm (with and without the residual add) and ris_swiglu against
+    their definitions, float32 and bf16."""
+    ris = need_gpu()
+    rng = np.random.default_rng(0)
+    for dt, tol in [(torch.float32, 2e-6), (torch.bfloat16, 2e-2)]:
+        x = torch.tensor(rng.standard_normal((37, 300)), dtype=dt, device="cuda")
+        r = torch.tensor(rng.standard_normal((37, 300)), dtype=dt, device="cuda")
+        w = torch.tensor(1 + 0.1 * rng.standard_normal(300), dtype=dt, device="cuda")
+        xs, rs, ws = (t.double().cpu().numpy() for t in (x, r, w))
+        out = torch.empty_like(x)
+        ris.rmsnorm(x, w, out, 1e-6)
+        np.testing.assert_allclose(out.double().cpu().numpy(), o_model.rmsnorm(xs, ws, 1e-6), atol=tol * 4)
+        res = r.clone()
+        ris.rmsnorm(x, w, out, 1e-6, residual=res)
+        summed = (x.double() + r.double()).to(dt).double().cpu().numpy()
+        assert np.array_equal(res.double().cpu().numpy(), summed)
+        np.testing.assert_allclose(out.double().cpu().numpy(), o_model.rmsnorm(summed, ws, 1e-6), atol=tol * 4)
+        gu = torch.tensor(rng.standard_normal((37, 2 * 300)), dtype=dt, device="cuda")
+        m = torch.empty(37, 300, dtype=dt, device="cuda")
+        ris.swiglu(gu, m)
+        g = gu.double().cpu().numpy()
+        np.testing.assert_allclose(m.double().cpu().numpy(), o_model.silu(g[:, :300]) * g[:, 300:], atol=tol * 4)
