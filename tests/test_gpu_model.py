@@ -10,7 +10,6 @@ bfloat16: activations are rounded to bf16 between every step (relative
 absolute on order-1 outputs over two layers, plus agreement in direction
 (cosine > 0.999).
 """
-from dataclasses import replace
 
 import numpy as np
 import pytest
