@@ -6,7 +6,8 @@
 // touch nearly every key block, so the work is a dense contraction under a
 // mask.  For every 64-key block the workgroup
 //   1. stages K[g, block] and V[g, block] in LDS, row-major, once for all
-//      32 rows x G heads;
+//      32 rows x G heads (double-buffered: block kb+1 is staged while block
+//      kb is computed, one workgroup barrier per block);
 //   2. turns each row's CSR entries that fall in the block into per-key tags
 //      in LDS (a window of 64 entries from the row's cursor suffices, the
 //      rows being ascending and unique);
@@ -100,12 +101,13 @@ __global__ __launch_bounds__(64 * G) void k_attn_tile32(AttnParams a, float c) {
     constexpr int VTASK = kKeys * (D / 8);          // 16-byte pieces of a V block
     constexpr int KPT = (KTASK + NT - 1) / NT;      // per thread
     constexpr int VPT = (VTASK + NT - 1) / NT;
-    __shared__ __align__(16) uint16_t Ks[kKeys * KS];
-    __shared__ __align__(16) uint16_t Vs[kKeys * VS];
-    __shared__ __align__(16) uint16_t tags[kTileRows * TS];
+    // Double-buffered: block kb+1 is staged while block kb is computed.
+    __shared__ __align__(16) uint16_t Ks_[2][kKeys * KS];
+    __shared__ __align__(16) uint16_t Vs_[2][kKeys * VS];
+    __shared__ __align__(16) uint16_t tags_[2][kTileRows * TS];
     __shared__ int64_t rstart_s[kTileRows];
     __shared__ int32_t rlen_s[kTileRows];
-    __shared__ int32_t wcount[G];
+    __shared__ int32_t any_s[2];
     __shared__ int32_t kb_range[2];
 
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -122,7 +124,8 @@ __global__ __launch_bounds__(64 * G) void k_attn_tile32(AttnParams a, float c) {
     if (!tile_is_dense(a, g, q0)) return;   // a sparse tile belongs to the gather kernel
 
     // ---- per-row CSR extents, tags cleared
-    for (int i = tid; i < kTileRows * TS; i += NT) tags[i] = 0;
+    for (int i = tid; i < 2 * kTileRows * TS; i += NT) (&tags_[0][0])[i] = 0;
+    if (tid < 2) any_s[tid] = 0;
     if (tid < kTileRows) {
         const int64_t q = q0 + tid;
         int64_t s = 0, L = 0;
@@ -208,12 +211,14 @@ __global__ __launch_bounds__(64 * G) void k_attn_tile32(AttnParams a, float c) {
             wreg[i] = lane < rln[i] - cur[i] ? a.col_idx[rst[i] + cur[i] + lane] : -1;
     };
 
-    if (kb_lo <= kb_hi) {
-        load_kv(kb_lo);
-        load_windows();
-    }
-    for (int kb = kb_lo; kb <= kb_hi; ++kb) {
+    // Stage block kb (its K/V pieces are in kreg/vreg, its CSR windows in
+    // wreg) into LDS buffer p, with its tags; the "any entries" flag of the
+    // buffer is stamped with kb + 1.
+    auto stage = [&](int kb, int p) {
         const int64_t k0 = (int64_t)kb * kKeys;
+        uint16_t* Ks = Ks_[p];
+        uint16_t* Vs = Vs_[p];
+        uint16_t* tags = tags_[p];
         // ---- registers -> LDS: K row-major, V transposed (keys of a pair side by side)
 #pragma unroll
         for (int u = 0; u < KPT; ++u) {
@@ -233,8 +238,6 @@ __global__ __launch_bounds__(64 * G) void k_attn_tile32(AttnParams a, float c) {
                 *reinterpret_cast<u32x4_t*>(&Vs[key * VS + ch * 8]) = v;
             }
         }
-        // ---- the next block's K/V loads fly from here until its staging
-        if (kb < kb_hi) load_kv(kb + 1);
         // ---- tags: keys of this block present in each row's set
         const uint16_t tag = (uint16_t)(kb + 1);
         int my_cnt = 0;
@@ -252,14 +255,34 @@ __global__ __launch_bounds__(64 * G) void k_attn_tile32(AttnParams a, float c) {
                 my_cnt += cnt;
             }
         }
-        if (lane == 0) wcount[w] = my_cnt;
-        __syncthreads();
-        // ---- next block's CSR windows (cursors are now past this block)
-        if (kb < kb_hi) load_windows();
-        int any = 0;
-#pragma unroll
-        for (int i = 0; i < G; ++i) any += wcount[i];
+        if (lane == 0 && my_cnt) any_s[p] = kb + 1;
+    };
 
+    if (kb_lo <= kb_hi) {
+        load_kv(kb_lo);
+        load_windows();
+        stage(kb_lo, kb_lo & 1);
+        if (kb_lo < kb_hi) {
+            load_kv(kb_lo + 1);
+            load_windows();
+        }
+    }
+    __syncthreads();
+    // One barrier per block (see k_attn_tile16).
+    for (int kb = kb_lo; kb <= kb_hi; ++kb) {
+        const int p = kb & 1;
+        if (kb < kb_hi) {
+            stage(kb + 1, p ^ 1);
+            if (kb + 1 < kb_hi) {
+                load_kv(kb + 2);
+                load_windows();
+            }
+        }
+        const uint16_t* Ks = Ks_[p];
+        const uint16_t* Vs = Vs_[p];
+        const uint16_t* tags = tags_[p];
+        const uint16_t tag = (uint16_t)(kb + 1);
+        const int any = any_s[p] == kb + 1;
         if (any) {
             // ---- S^T[key, query] = K_blk Q_h^T
             f32x16_t st[2];
@@ -385,9 +408,10 @@ __global__ __launch_bounds__(128 * G) void k_attn_tile16(AttnParams a, float c) 
     constexpr int DT = D / 16;                       // 16-dim tiles of the output
     constexpr int PIECES = kKeys * (D / 8);          // 16-byte pieces of a K (or V) block
     constexpr int PPT = (PIECES + NT - 1) / NT;      // per thread
-    __shared__ __align__(16) uint16_t Ks[kKeys * KS];
-    __shared__ __align__(16) uint16_t Vs[kKeys * VS];
-    __shared__ __align__(16) uint16_t tags[kTileRows * TS];
+    // Double-buffered: block kb+1 is staged while block kb is computed.
+    __shared__ __align__(16) uint16_t Ks_[2][kKeys * KS];
+    __shared__ __align__(16) uint16_t Vs_[2][kKeys * VS];
+    __shared__ __align__(16) uint16_t tags_[2][kTileRows * TS];
     __shared__ int64_t rstart_s[kTileRows];
     __shared__ int32_t rlen_s[kTileRows];
     __shared__ int32_t any_s[2];
@@ -409,7 +433,7 @@ __global__ __launch_bounds__(128 * G) void k_attn_tile16(AttnParams a, float c) 
     if (!tile_is_dense(a, g, q0)) return;   // a sparse tile belongs to the gather kernel
 
     // ---- per-row CSR extents, tags cleared
-    for (int i = tid; i < kTileRows * TS; i += NT) tags[i] = 0;
+    for (int i = tid; i < 2 * kTileRows * TS; i += NT) (&tags_[0][0])[i] = 0;
     if (tid < 2) any_s[tid] = 0;
     if (tid < kTileRows) {
         const int64_t q = q0 + tid;
@@ -493,13 +517,14 @@ __global__ __launch_bounds__(128 * G) void k_attn_tile16(AttnParams a, float c) 
             wreg[i] = lane < rln[i] - cur[i] ? a.col_idx[rst[i] + cur[i] + lane] : -1;
     };
 
-    if (kb_lo <= kb_hi) {
-        load_kv(kb_lo);
-        load_windows();
-    }
-    for (int kb = kb_lo; kb <= kb_hi; ++kb) {
+    // Stage block kb (its K/V pieces are in kreg/vreg, its CSR windows in
+    // wreg) into LDS buffer p, with its tags; the "any entries" flag of the
+    // buffer is stamped with kb + 1.
+    auto stage = [&](int kb, int p) {
         const int64_t k0 = (int64_t)kb * kKeys;
-        // ---- registers -> LDS, both row-major
+        uint16_t* Ks = Ks_[p];
+        uint16_t* Vs = Vs_[p];
+        uint16_t* tags = tags_[p];
 #pragma unroll
         for (int u = 0; u < PPT; ++u) {
             const int e = tid + u * NT;
@@ -511,9 +536,6 @@ __global__ __launch_bounds__(128 * G) void k_attn_tile16(AttnParams a, float c) 
                 *reinterpret_cast<u32x4_t*>(&Vs[key * VS + ch * 8]) = v;
             }
         }
-        // ---- the next block's K/V loads fly from here until its staging
-        if (kb < kb_hi) load_kv(kb + 1);
-        // ---- tags: keys of this block present in each row's set
         const uint16_t tag = (uint16_t)(kb + 1);
         int my_cnt = 0;
 #pragma unroll
@@ -530,13 +552,36 @@ __global__ __launch_bounds__(128 * G) void k_attn_tile16(AttnParams a, float c) 
                 my_cnt += cnt;
             }
         }
-        if (lane == 0 && my_cnt) any_s[kb & 1] = 1;
-        __syncthreads();
-        // ---- next block's CSR windows (cursors are now past this block)
-        if (kb < kb_hi) load_windows();
-        const int any = any_s[kb & 1];
-        if (tid == 0) any_s[(kb + 1) & 1] = 0;
+        if (lane == 0 && my_cnt) any_s[p] = kb + 1;
+    };
 
+    if (kb_lo <= kb_hi) {
+        load_kv(kb_lo);
+        load_windows();
+        stage(kb_lo, kb_lo & 1);
+        if (kb_lo < kb_hi) {
+            load_kv(kb_lo + 1);
+            load_windows();
+        }
+    }
+    __syncthreads();
+    // One barrier per block: at iteration kb the workgroup stages block kb+1
+    // into the other buffer (last read during iteration kb-1, before the
+    // previous barrier) and computes block kb (staged before it).
+    for (int kb = kb_lo; kb <= kb_hi; ++kb) {
+        const int p = kb & 1;
+        if (kb < kb_hi) {
+            stage(kb + 1, p ^ 1);
+            if (kb + 1 < kb_hi) {
+                load_kv(kb + 2);
+                load_windows();
+            }
+        }
+        const uint16_t* Ks = Ks_[p];
+        const uint16_t* Vs = Vs_[p];
+        const uint16_t* tags = tags_[p];
+        const uint16_t tag = (uint16_t)(kb + 1);
+        const int any = any_s[p] == kb + 1;
         if (any) {
             // ---- S^T[key, query] = K_blk Q_h^T; st[kt][i] is key 16 kt + 4 (l/16) + i
             f32x4_t st[4];
