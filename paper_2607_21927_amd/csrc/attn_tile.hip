@@ -60,17 +60,6 @@ __device__ __forceinline__ bf16x8_t as_bf16x8(u32x4_t v) {
     return __builtin_bit_cast(bf16x8_t, v);
 }
 
-// max / sum of x over this lane and the lane 32 away (v_permlane32_swap:
-// with both operands x, the two results hold x at lanes l and l^32).
-__device__ __forceinline__ float pair_max32(float x) {
-    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
-}
-__device__ __forceinline__ float pair_sum32(float x) {
-    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
-}
-
 // v if keep, else zeros (the load itself always reads a valid address).
 __device__ __forceinline__ uint4 select4(bool keep, uint4 v) {
     return keep ? v : make_uint4(0u, 0u, 0u, 0u);
@@ -608,8 +597,7 @@ __global__ __launch_bounds__(128 * G) void k_attn_tile16(AttnParams a, float c) 
                     mx = fmaxf(mx, s);
                 }
             }
-            mx = fmaxf(mx, __shfl_xor(mx, 16));
-            mx = fmaxf(mx, __shfl_xor(mx, 32));
+            mx = quad_max16(mx);
             const float m_new = fmaxf(m_run, mx);
             const float m_use = m_new == -INFINITY ? 0.f : m_new;
             const float mc = m_use * c;
@@ -656,8 +644,7 @@ __global__ __launch_bounds__(128 * G) void k_attn_tile16(AttnParams a, float c) 
     }
 
     // ---- normalise and store: o[dt][i] is dim 16 dt + 4 (l/16) + i of the query
-    l_run += __shfl_xor(l_run, 16);
-    l_run += __shfl_xor(l_run, 32);
+    l_run = quad_sum16(l_run);
     const int64_t q = q0 + qr;
     if (q < N) {
         const float inv = l_run > 0.f ? 1.0f / l_run : 0.f;

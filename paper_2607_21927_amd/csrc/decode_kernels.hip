@@ -194,8 +194,7 @@ __global__ __launch_bounds__(64 * kDecodeWaves, 2) void k_decode_partial(DecodeP
                     sc[kb][i] = ok ? st[kb][i] * c : -INFINITY;
                     mx = fmaxf(mx, sc[kb][i]);
                 }
-            mx = fmaxf(mx, __shfl_xor(mx, 16));
-            mx = fmaxf(mx, __shfl_xor(mx, 32));
+            mx = quad_max16(mx);
             const float m_new = fmaxf(m_run, mx);
             const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
             float pv[2][4];
@@ -238,8 +237,7 @@ __global__ __launch_bounds__(64 * kDecodeWaves, 2) void k_decode_partial(DecodeP
     }
 
     // ---- this wave's partial
-    l_run += __shfl_xor(l_run, 16);
-    l_run += __shfl_xor(l_run, 32);
+    l_run = quad_sum16(l_run);
     const int64_t slot = (int64_t)row * p.parts + part;
     float* pml = p.part_ml + slot * G * 2;
     if (lane < G) {

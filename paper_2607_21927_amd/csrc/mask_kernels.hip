@@ -75,17 +75,22 @@ __device__ __forceinline__ void walk_draws(const FeistelDomain& dom, const uint3
                                            float inv_draws) {
     uint32_t idx = threadIdx.x;
     uint32_t x = 0, steps = 0;
+    int s = 0, j = 0;
     uint32_t w[kRowWords];
-    auto start = [&]() {
-        int s, j;
-        split_draw(idx, draws, inv_draws, s, j);
-        x = (uint32_t)j;
+    auto load_words = [&]() {
         const u32x4_t w0 = *reinterpret_cast<const u32x4_t*>(&rks[s * kRowWords]);
         const u32x4_t w1 = *reinterpret_cast<const u32x4_t*>(&rks[s * kRowWords + 4]);
         w[0] = w0.x; w[1] = w0.y; w[2] = w0.z; w[3] = w0.w;
         w[4] = w1.x; w[5] = w1.y; w[6] = w1.z; w[7] = w1.w;
     };
-    if (idx < total) start();
+    // With at least kThreads draws per seed the next pair of a lane is its
+    // draw index plus kThreads, wrapping at most once into the next seed.
+    const bool incremental = draws >= (uint32_t)kThreads;
+    if (idx < total) {
+        split_draw(idx, draws, inv_draws, s, j);
+        x = (uint32_t)j;
+        load_words();
+    }
     while (idx < total) {
         x = feistel<ROUNDS>(x, w, dom.a, dom.b);
         ++steps;
@@ -94,7 +99,20 @@ __device__ __forceinline__ void walk_draws(const FeistelDomain& dom, const uint3
             atomicOr(&bits[x >> 5], 1u << (x & 31u));
             idx += kThreads;
             steps = 0;
-            if (idx < total) start();
+            if (idx < total) {
+                if (incremental) {
+                    j += kThreads;
+                    if (j >= (int)draws) {
+                        j -= (int)draws;
+                        ++s;
+                        load_words();
+                    }
+                } else {
+                    split_draw(idx, draws, inv_draws, s, j);
+                    load_words();
+                }
+                x = (uint32_t)j;
+            }
         }
     }
 }

@@ -117,6 +117,33 @@ __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
 }
 
 // ---------------------------------------------------------------------------
+// Exchanges between the lanes l, l^16, l^32, l^48 (gfx950 permlane swaps).
+// ---------------------------------------------------------------------------
+
+// max / sum of x over this lane and the lane 32 away (v_permlane32_swap:
+// with both operands x, the two results hold x at lanes l and l^32).
+__device__ __forceinline__ float pair_max32(float x) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float pair_sum32(float x) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+// max / sum of x over the four lanes l, l^16, l^32, l^48 (v_permlane16_swap
+// and v_permlane32_swap: with both operands x, lanes l and l^16 -- or l^32 --
+// receive the pair {x[l], x[l^16]}).
+__device__ __forceinline__ float quad_max16(float x) {
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return pair_max32(fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1])));
+}
+__device__ __forceinline__ float quad_sum16(float x) {
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return pair_sum32(__uint_as_float(r[0]) + __uint_as_float(r[1]));
+}
+
+// ---------------------------------------------------------------------------
 // Wavefront (64-lane) reductions via DPP; every lane receives the result.
 // ---------------------------------------------------------------------------
 
