@@ -497,8 +497,7 @@ def main():
         "hbm_gbs_attn": achieved,
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
-                     "kernel": (f"k_attn_tile{16 if w.D == 128 else 32}<{w.D}, {G}>" if tiled
-                                else f"k_attn_gather<{w.D}>"),
+                     "kernel": f"k_attn_tile16<{w.D}, {G}>" if tiled else f"k_attn_gather<{w.D}>",
                      "bytes_per_kv_pair": KV_PAIR_BYTES[w.D]},
         # The tiled kernel reads each K/V block once per 32 rows, so its real
         # bound is matrix/vector work: the method's flops (4 D G per kv-pair:

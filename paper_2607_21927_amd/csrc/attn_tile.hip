@@ -1,5 +1,6 @@
 // Sparse attention, tiled form: one workgroup per (kv_head g, 32 consecutive
-// query rows).
+// query rows), two wavefronts per query head of the GQA group (one per half
+// of the 32 rows).
 //
 // When a row's unified set covers a sizeable share of its keys (a 70-seed
 // ensemble at 1% reaches ~50%), the sets of 32 neighbouring rows together
@@ -11,25 +12,21 @@
 //   2. turns each row's CSR entries that fall in the block into per-key tags
 //      in LDS (a window of 64 entries from the row's cursor suffices, the
 //      rows being ascending and unique);
-//   3. per wave: S^T = K_blk Q^T on MFMA, masked by the tags, one
-//      online-softmax update per query over the block, and O^T += V_blk^T P^T
-//      on MFMA with P kept in registers and V^T read from the row-major block
-//      with the LDS transpose read (ds_read_b64_tr_b16).
-// Every index of a row's set enters one normalisation (Pre-Fusion Unified
-// Softmax; Methods, "Hybrid Anchor and Pre-Fusion Unified Softmax").  In
-// Structural mode the block clique is the diagonal 64-key block: the dense
-// local tile runs on MFMA in the same softmax state as the sampled global keys.
+//   3. per wave (head h, 16 rows): S^T = K_blk Q^T on MFMA (16x16x32 bf16),
+//      masked by the tags, one online-softmax update per query over the
+//      block, and O^T += V_blk^T P^T on MFMA with P kept in registers and V^T
+//      read from the row-major block with the LDS transpose read
+//      (ds_read_b64_tr_b16).
+// In both products lane l holds query l % 16 (keys or dims 4 (l/16) + i of
+// each 16-wide tile), so the rescale needs no exchange and a query's running
+// max and sum live in four lanes (permlane swaps combine them).  Every index
+// of a row's set enters one normalisation (Pre-Fusion Unified Softmax;
+// Methods, "Hybrid Anchor and Pre-Fusion Unified Softmax").  In Structural
+// mode the block clique is the diagonal 64-key block: the dense local tile
+// runs on MFMA in the same softmax state as the sampled global keys.
 //
-// Two wave layouts, chosen by head dimension (measured on MI355X):
-//   * D = 128: k_attn_tile16 -- two waves per query head, 16 query rows each,
-//     MFMA 16x16x32.  A wave holds ~150 VGPRs, so the 2G waves of the
-//     workgroup sit three to a SIMD and the MFMA work of one wave overlaps the
-//     softmax of another; lane l holds query l % 16 in both products, so a
-//     query's running max and sum live in four lanes.
-//   * D = 64: k_attn_tile32 -- one wave per query head, all 32 rows, MFMA
-//     32x32x16; lane l holds query l % 32 and exchanges with lane l ^ 32.
-//     At D = 64 the 16-row layout doubles the LDS reads per MFMA flop and
-//     loses.
+// 2G waves of at most ~170 VGPRs sit three or four to a SIMD: the MFMA work
+// of one wave overlaps the softmax of another.
 #include "ris_device.h"
 #include "ris_internal.h"
 
@@ -37,7 +34,6 @@ namespace ris {
 namespace {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
-typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 typedef short s16x4_t __attribute__((ext_vector_type(4)));
 
@@ -53,16 +49,8 @@ __device__ __forceinline__ uint2 lds_read_tr16(const uint16_t* p) {
 
 constexpr int kKeys = 64;   // keys per block
 
-__device__ __forceinline__ bf16x8_t as_bf16x8(uint4 v) {
-    return __builtin_bit_cast(bf16x8_t, v);
-}
 __device__ __forceinline__ bf16x8_t as_bf16x8(u32x4_t v) {
     return __builtin_bit_cast(bf16x8_t, v);
-}
-
-// v if keep, else zeros (the load itself always reads a valid address).
-__device__ __forceinline__ uint4 select4(bool keep, uint4 v) {
-    return keep ? v : make_uint4(0u, 0u, 0u, 0u);
 }
 
 typedef float f32x2_t __attribute__((ext_vector_type(2)));
@@ -75,314 +63,6 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
 }
 
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
-
-template <int D, int G>
-__global__ __launch_bounds__(64 * G) void k_attn_tile32(AttnParams a, float c) {
-    constexpr int NT = 64 * G;
-    constexpr int KS = D + 8;          // K row stride in LDS (bf16 elements)
-    constexpr int VS = D + 16;         // V row stride: the 4 rows a 16-lane transpose read
-                                       // touches start 8 banks apart
-    constexpr int TS = kKeys + 4;      // tag row stride
-    constexpr int RPW = (kTileRows + G - 1) / G;
-    constexpr int KSTEPS = D / 16;
-    constexpr int DT = D / 32;
-    constexpr int KTASK = kKeys * (D / 8);          // 16-byte pieces of a K block
-    constexpr int VTASK = kKeys * (D / 8);          // 16-byte pieces of a V block
-    constexpr int KPT = (KTASK + NT - 1) / NT;      // per thread
-    constexpr int VPT = (VTASK + NT - 1) / NT;
-    // Double-buffered: block kb+1 is staged while block kb is computed.
-    __shared__ __align__(16) uint16_t Ks_[2][kKeys * KS];
-    __shared__ __align__(16) uint16_t Vs_[2][kKeys * VS];
-    __shared__ __align__(16) uint16_t tags_[2][kTileRows * TS];
-    __shared__ int64_t rstart_s[kTileRows];
-    __shared__ int32_t rlen_s[kTileRows];
-    __shared__ int32_t any_s[2];
-    __shared__ int32_t kb_range[2];
-
-    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-    const int hf = lane >> 5, n = lane & 31;
-    const int64_t N = a.N;
-    const int64_t tiles = (N + kTileRows - 1) / kTileRows;
-    const int64_t bid = blockIdx.x;
-    const int64_t tile = tiles - 1 - bid / a.Hkv;     // late (heavy) tiles first
-    const int g = (int)(bid % a.Hkv);
-    const int64_t q0 = tile * kTileRows;
-    const int h = g * G + w;
-    const uint16_t* Kg = static_cast<const uint16_t*>(a.K) + (int64_t)g * N * D;
-    const uint16_t* Vg = static_cast<const uint16_t*>(a.V) + (int64_t)g * N * D;
-    if (!tile_is_dense(a, g, q0)) return;   // a sparse tile belongs to the gather kernel
-
-    // ---- per-row CSR extents, tags cleared
-    for (int i = tid; i < 2 * kTileRows * TS; i += NT) (&tags_[0][0])[i] = 0;
-    if (tid < 2) any_s[tid] = 0;
-    if (tid < kTileRows) {
-        const int64_t q = q0 + tid;
-        int64_t s = 0, L = 0;
-        if (q < N) {
-            s = a.row_ptr[g * N + q];
-            L = a.row_ptr[g * N + q + 1] - s;
-        }
-        rstart_s[tid] = s;
-        rlen_s[tid] = (int)L;
-    }
-    __syncthreads();
-    // Key-block range touched by any row: first and last entries of each row.
-    if (w == 0) {
-        int lo = 0x7FFFFFFF, hi = -1;
-        if (lane < kTileRows && rlen_s[lane] > 0) {
-            const int64_t nb = (N - 1) / kKeys;
-            int64_t f = a.col_idx[rstart_s[lane]] / kKeys;
-            int64_t l = a.col_idx[rstart_s[lane] + rlen_s[lane] - 1] / kKeys;
-            f = f < 0 ? 0 : (f > nb ? nb : f);
-            l = l < 0 ? 0 : (l > nb ? nb : l);
-            lo = (int)f;
-            hi = (int)l;
-        }
-        for (int off = 32; off > 0; off >>= 1) {
-            lo = min(lo, __shfl_xor(lo, off));
-            hi = max(hi, __shfl_xor(hi, off));
-        }
-        if (lane == 0) { kb_range[0] = lo; kb_range[1] = hi; }
-    }
-
-    // ---- this lane's query row of Q_h, as the B operand (k = dims)
-    bf16x8_t qf[KSTEPS];
-    {
-        const int64_t q = q0 + n;
-        const uint16_t* Qrow = static_cast<const uint16_t*>(a.Q) + ((int64_t)h * N + (q < N ? q : 0)) * D;
-#pragma unroll
-        for (int ks = 0; ks < KSTEPS; ++ks)
-            qf[ks] = as_bf16x8(select4(q < N, *reinterpret_cast<const uint4*>(Qrow + ks * 16 + 8 * hf)));
-    }
-    float m_run = -INFINITY, l_run = 0.f;
-    f32x16_t o[DT];
-#pragma unroll
-    for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) o[dt][r] = 0.f;
-    __syncthreads();
-
-    // Rows this wave turns into tags: r = w + G*i.
-    int64_t rst[RPW];
-    int rln[RPW], cur[RPW];
-#pragma unroll
-    for (int i = 0; i < RPW; ++i) {
-        const int r = w + G * i;
-        rst[i] = r < kTileRows ? rstart_s[r] : 0;
-        rln[i] = r < kTileRows ? rlen_s[r] : 0;
-        cur[i] = 0;
-    }
-    const int kb_lo = kb_range[0], kb_hi = kb_range[1];
-
-    // ---- register staging of one block (K pieces, V pair pieces, CSR windows)
-    u32x4_t kreg[KPT], vreg[VPT];
-    int wreg[RPW];
-    auto load_kv = [&](int kb) {
-        const int k0 = kb * kKeys;
-#pragma unroll
-        for (int u = 0; u < KPT; ++u) {
-            const int e = tid + u * NT;
-            const int key = e / (D / 8), ch = e % (D / 8);
-            const int64_t j = min(k0 + key, (int)N - 1);   // rows past N are masked out
-            if (KTASK % NT == 0 || e < KTASK) kreg[u] = *reinterpret_cast<const u32x4_t*>(Kg + j * D + ch * 8);
-        }
-#pragma unroll
-        for (int u = 0; u < VPT; ++u) {
-            const int e = tid + u * NT;
-            const int key = e / (D / 8), ch = e % (D / 8);
-            const int64_t j = min(k0 + key, (int)N - 1);
-            if (VTASK % NT == 0 || e < VTASK) vreg[u] = *reinterpret_cast<const u32x4_t*>(Vg + j * D + ch * 8);
-        }
-    };
-    auto load_windows = [&]() {
-#pragma unroll
-        for (int i = 0; i < RPW; ++i)
-            wreg[i] = lane < rln[i] - cur[i] ? a.col_idx[rst[i] + cur[i] + lane] : -1;
-    };
-
-    // Stage block kb (its K/V pieces are in kreg/vreg, its CSR windows in
-    // wreg) into LDS buffer p, with its tags; the "any entries" flag of the
-    // buffer is stamped with kb + 1.
-    auto stage = [&](int kb, int p) {
-        const int64_t k0 = (int64_t)kb * kKeys;
-        uint16_t* Ks = Ks_[p];
-        uint16_t* Vs = Vs_[p];
-        uint16_t* tags = tags_[p];
-        // ---- registers -> LDS: K row-major, V transposed (keys of a pair side by side)
-#pragma unroll
-        for (int u = 0; u < KPT; ++u) {
-            const int e = tid + u * NT;
-            if (KTASK % NT == 0 || e < KTASK) {
-                const int key = e / (D / 8), ch = e % (D / 8);
-                *reinterpret_cast<u32x4_t*>(&Ks[key * KS + ch * 8]) = kreg[u];   // rows past N: masked
-            }
-        }
-#pragma unroll
-        for (int u = 0; u < VPT; ++u) {
-            const int e = tid + u * NT;
-            if (VTASK % NT == 0 || e < VTASK) {
-                const int key = e / (D / 8), ch = e % (D / 8);
-                u32x4_t v = vreg[u];
-                if (k0 + key >= N) v = u32x4_t{0u, 0u, 0u, 0u};   // V rows past N read as zeros
-                *reinterpret_cast<u32x4_t*>(&Vs[key * VS + ch * 8]) = v;
-            }
-        }
-        // ---- tags: keys of this block present in each row's set
-        const uint16_t tag = (uint16_t)(kb + 1);
-        int my_cnt = 0;
-#pragma unroll
-        for (int i = 0; i < RPW; ++i) {
-            const int r = w + G * i;
-            if (r < kTileRows) {
-                const int col = wreg[i];
-                const int k0i = kb * kKeys;
-                const bool inb = col >= k0i && col < k0i + kKeys && col < (int)N;
-                const uint64_t bal = __ballot(inb);
-                if (inb) tags[r * TS + (col - k0i)] = tag;
-                const int cnt = __popcll(bal);
-                cur[i] += cnt;
-                my_cnt += cnt;
-            }
-        }
-        if (lane == 0 && my_cnt) any_s[p] = kb + 1;
-    };
-
-    if (kb_lo <= kb_hi) {
-        load_kv(kb_lo);
-        load_windows();
-        stage(kb_lo, kb_lo & 1);
-        if (kb_lo < kb_hi) {
-            load_kv(kb_lo + 1);
-            load_windows();
-        }
-    }
-    __syncthreads();
-    // One barrier per block (see k_attn_tile16).
-    for (int kb = kb_lo; kb <= kb_hi; ++kb) {
-        const int p = kb & 1;
-        if (kb < kb_hi) {
-            stage(kb + 1, p ^ 1);
-            if (kb + 1 < kb_hi) {
-                load_kv(kb + 2);
-                load_windows();
-            }
-        }
-        const uint16_t* Ks = Ks_[p];
-        const uint16_t* Vs = Vs_[p];
-        const uint16_t* tags = tags_[p];
-        const uint16_t tag = (uint16_t)(kb + 1);
-        const int any = any_s[p] == kb + 1;
-        if (any) {
-            // ---- S^T[key, query] = K_blk Q_h^T
-            f32x16_t st[2];
-#pragma unroll
-            for (int t = 0; t < 2; ++t) {
-#pragma unroll
-                for (int r = 0; r < 16; ++r) st[t][r] = 0.f;
-#pragma unroll
-                for (int ks = 0; ks < KSTEPS; ++ks) {
-                    const bf16x8_t av =
-                        as_bf16x8(*reinterpret_cast<const uint4*>(&Ks[(32 * t + n) * KS + ks * 16 + 8 * hf]));
-                    st[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, qf[ks], st[t], 0, 0, 0);
-                }
-            }
-            // ---- mask, one online-softmax step for this lane's query
-            // st[t][4i + j] holds key 32t + 8i + 4hf + j of query n.
-            float mx = -INFINITY;
-#pragma unroll
-            for (int t = 0; t < 2; ++t) {
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const uint2 tg = *reinterpret_cast<const uint2*>(&tags[n * TS + 32 * t + 8 * i + 4 * hf]);
-                    const uint32_t tv[4] = {tg.x & 0xFFFFu, tg.x >> 16, tg.y & 0xFFFFu, tg.y >> 16};
-#pragma unroll
-                    for (int j = 0; j < 4; ++j) {
-                        const float s = tv[j] == tag ? st[t][4 * i + j] : -INFINITY;
-                        st[t][4 * i + j] = s;
-                        mx = fmaxf(mx, s);
-                    }
-                }
-            }
-            mx = pair_max32(mx);
-            const float m_new = fmaxf(m_run, mx);
-            const float m_use = m_new == -INFINITY ? 0.f : m_new;
-            const float mc = m_use * c;
-            float rs = 0.f;
-#pragma unroll
-            for (int t = 0; t < 2; ++t)
-#pragma unroll
-                for (int r = 0; r < 16; ++r) {
-                    const float p = __builtin_amdgcn_exp2f(fmaf(st[t][r], c, -mc));
-                    st[t][r] = p;
-                    rs += p;
-                }
-            rs = pair_sum32(rs);
-            if (__ballot(m_new != m_run) != 0ull) {      // some query's max moved: rescale
-                const float corr = __builtin_amdgcn_exp2f(fmaf(m_run, c, -mc));
-                l_run *= corr;
-#pragma unroll
-                for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-                    for (int r = 0; r < 16; ++r) o[dt][r] *= corr;
-            }
-            l_run += rs;
-            m_run = m_new;
-            // ---- P^T as the B operand: k-step (t, u) holds keys
-            // 32t+16u+4hf+{0..3} and 32t+16u+8+4hf+{0..3}
-            bf16x8_t pb[2][2];
-#pragma unroll
-            for (int t = 0; t < 2; ++t)
-#pragma unroll
-                for (int u = 0; u < 2; ++u) {
-                    uint4 pk;
-                    pk.x = pack_bf16x2(st[t][8 * u + 0], st[t][8 * u + 1]);
-                    pk.y = pack_bf16x2(st[t][8 * u + 2], st[t][8 * u + 3]);
-                    pk.z = pack_bf16x2(st[t][8 * u + 4], st[t][8 * u + 5]);
-                    pk.w = pack_bf16x2(st[t][8 * u + 6], st[t][8 * u + 7]);
-                    pb[t][u] = as_bf16x8(pk);
-                }
-            // ---- O^T[d, query] += V_blk^T P^T
-#pragma unroll
-            for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-                for (int t = 0; t < 2; ++t)
-#pragma unroll
-                    for (int u = 0; u < 2; ++u) {
-                        // lane i of each 16-lane group: dim 32dt + 16*((lane/16)&1) + i,
-                        // keys 32t+16u+4hf+{0..3} (lo) and +8 (hi), as P^T holds them
-                        const uint16_t* vp = &Vs[(32 * t + 16 * u + 4 * hf + ((lane & 15) >> 2)) * VS +
-                                                 32 * dt + 16 * ((lane >> 4) & 1) + 4 * (lane & 3)];
-                        const uint2 lo = lds_read_tr16(vp);
-                        const uint2 hi = lds_read_tr16(vp + 8 * VS);
-                        const bf16x8_t av = as_bf16x8(make_uint4(lo.x, lo.y, hi.x, hi.y));
-                        o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pb[t][u], o[dt], 0, 0, 0);
-                    }
-        }
-        __syncthreads();
-    }
-
-    // ---- normalise and store: o[dt][r] is dim 32dt + 8(r/4) + 4hf + r%4 of query n
-    const int64_t q = q0 + n;
-    if (q < N) {
-        const float inv = l_run > 0.f ? 1.0f / l_run : 0.f;
-        const int64_t base = ((int64_t)h * N + q) * D;
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int d = 32 * dt + 8 * i + 4 * hf;
-                const float v0 = o[dt][4 * i] * inv, v1 = o[dt][4 * i + 1] * inv;
-                const float v2 = o[dt][4 * i + 2] * inv, v3 = o[dt][4 * i + 3] * inv;
-                if (a.out_bf16) {
-                    *reinterpret_cast<uint2*>(static_cast<uint16_t*>(a.out) + base + d) =
-                        make_uint2(pack_bf16x2(v0, v1), pack_bf16x2(v2, v3));
-                } else {
-                    *reinterpret_cast<float4*>(static_cast<float*>(a.out) + base + d) =
-                        make_float4(v0, v1, v2, v3);
-                }
-            }
-    }
-}
 
 template <int D, int G>
 __global__ __launch_bounds__(128 * G) void k_attn_tile16(AttnParams a, float c) {
@@ -669,10 +349,7 @@ template <int D, int G>
 hipError_t launch_d_g(const AttnParams& a, float c, hipStream_t st) {
     const int64_t tiles = (a.N + kTileRows - 1) / kTileRows;
     const dim3 grid((unsigned)(tiles * a.Hkv));
-    if constexpr (D == 128)
-        hipLaunchKernelGGL((k_attn_tile16<D, G>), grid, dim3(128 * G), 0, st, a, c);
-    else
-        hipLaunchKernelGGL((k_attn_tile32<D, G>), grid, dim3(64 * G), 0, st, a, c);
+    hipLaunchKernelGGL((k_attn_tile16<D, G>), grid, dim3(128 * G), 0, st, a, c);
     return hipGetLastError();
 }
 
