@@ -100,6 +100,24 @@ def cpu_baseline(w, layer, Q, K, V, workers, stride):
 # ---------------------------------------------------------------------------
 # GPU
 # ---------------------------------------------------------------------------
+def stream_copy_gbs(torch, nbytes=1 << 30, reps=10):
+    """Measured device-to-device copy bandwidth (bytes read + written per
+    second, GB/s) of a 1 GiB buffer: the practical HBM ceiling."""
+    a = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    b = torch.empty_like(a)
+    b.copy_(a)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        b.copy_(a)
+    e1.record()
+    torch.cuda.synchronize()
+    gbs = 2 * nbytes * reps / (e0.elapsed_time(e1) * 1e-3) / 1e9
+    del a, b
+    return gbs
+
+
 def run_gpu(w, layers, Q, K, V, steps, warmup, algo):
     import torch
     from paper_2607_21927_amd import ris
@@ -172,7 +190,8 @@ def run_gpu(w, layers, Q, K, V, steps, warmup, algo):
             nnz = [int(row_ptr[-1].item())]
         else:
             raise SystemExit("several layers need at least one warm-up step (it records nnz)")
-    return dict(ms_step=total_ms / steps, ms_rope=t_rope / steps, ms_mask=t_mask / steps,
+    copy_gbs = stream_copy_gbs(torch)
+    return dict(copy_gbs=copy_gbs, ms_step=total_ms / steps, ms_rope=t_rope / steps, ms_mask=t_mask / steps,
                 ms_attn=t_attn / steps, nnz=sum(nnz), layers=len(descs))
 
 
@@ -498,6 +517,7 @@ def main():
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
                      "kernel": f"k_attn_tile16<{w.D}, {G}>" if tiled else f"k_attn_gather<{w.D}>",
+                     "measured_copy_gbs": g["copy_gbs"], "frac_of_measured_copy": achieved / g["copy_gbs"],
                      "bytes_per_kv_pair": KV_PAIR_BYTES[w.D]},
         # The tiled kernel reads each K/V block once per 32 rows, so its real
         # bound is matrix/vector work: the method's flops (4 D G per kv-pair:
