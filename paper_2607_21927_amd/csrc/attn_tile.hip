@@ -9,23 +9,29 @@
 //   1. stages K[g, block] and V[g, block] in LDS, row-major, once for all
 //      32 rows x G heads (double-buffered: block kb+1 is staged while block
 //      kb is computed, one workgroup barrier per block);
-//   2. turns each row's CSR entries that fall in the block into per-key tags
-//      in LDS (a window of 64 entries from the row's cursor suffices, the
-//      rows being ascending and unique);
-//   3. per wave (head h, 16 rows): S^T = K_blk Q^T on MFMA (16x16x32 bf16),
-//      masked by the tags, one online-softmax update per query over the
+//   2. turns each row's CSR entries that fall in the block into a score
+//      bias in LDS, 0 at the row's keys and -inf elsewhere (a window of 64
+//      entries from the row's cursor suffices, the rows being ascending and
+//      unique);
+//   3. per wave (head h, 16 rows): S^T = bias + K_blk Q^T on MFMA (16x16x32
+//      bf16; the bias is the initial accumulator, so masking costs no
+//      vector instructions), one online-softmax update per query over the
 //      block, and O^T += V_blk^T P^T on MFMA with P kept in registers and V^T
 //      read from the row-major block with the LDS transpose read
-//      (ds_read_b64_tr_b16).
+//      (ds_read_b64_tr_b16); the row sums of P come from the same product
+//      with an all-ones A operand, so numerator and denominator use the
+//      same bf16 weights.
 // In both products lane l holds query l % 16 (keys or dims 4 (l/16) + i of
 // each 16-wide tile), so the rescale needs no exchange and a query's running
-// max and sum live in four lanes (permlane swaps combine them).  Every index
-// of a row's set enters one normalisation (Pre-Fusion Unified Softmax;
-// Methods, "Hybrid Anchor and Pre-Fusion Unified Softmax").  In Structural
-// mode the block clique is the diagonal 64-key block: the dense local tile
-// runs on MFMA in the same softmax state as the sampled global keys.
+// max lives in four lanes (permlane swaps combine them).  The reference max
+// moves only when a block's max exceeds it by more than kSlack (log2 units),
+// so rescales of O are rare.  Every index of a row's set enters one
+// normalisation (Pre-Fusion Unified Softmax; Methods, "Hybrid Anchor and
+// Pre-Fusion Unified Softmax").  In Structural mode the block clique is the
+// diagonal 64-key block: the dense local tile runs on MFMA in the same
+// softmax state as the sampled global keys.
 //
-// 2G waves of at most ~170 VGPRs sit three or four to a SIMD: the MFMA work
+// 2G waves of at most ~150 VGPRs sit three or four to a SIMD: the MFMA work
 // of one wave overlaps the softmax of another.
 #include "ris_device.h"
 #include "ris_internal.h"
@@ -48,6 +54,7 @@ __device__ __forceinline__ uint2 lds_read_tr16(const uint16_t* p) {
 }
 
 constexpr int kKeys = 64;   // keys per block
+constexpr float kSlack = 8.0f;
 
 __device__ __forceinline__ bf16x8_t as_bf16x8(u32x4_t v) {
     return __builtin_bit_cast(bf16x8_t, v);
@@ -71,8 +78,8 @@ __global__ __launch_bounds__(128 * G) void k_attn_tile16(AttnParams a, float c) 
     constexpr int KS = D + 16;          // K row stride in LDS (bf16 elements)
     constexpr int VS = D + 16;         // V row stride: the 4 rows a 16-lane transpose read
                                        // touches start 8 banks apart
-    constexpr int TS = kKeys + 4;      // tag row stride
-    constexpr int RPW = (kTileRows + NW - 1) / NW;       // tag rows per wave
+    constexpr int BS = kKeys + 4;      // bias row stride (floats)
+    constexpr int RPW = (kTileRows + NW - 1) / NW;       // bias rows per wave
     constexpr int KSL = D / 32;                      // k-steps of the score product
     constexpr int DT = D / 16;                       // 16-dim tiles of the output
     constexpr int PIECES = kKeys * (D / 8);          // 16-byte pieces of a K (or V) block
@@ -80,7 +87,12 @@ __global__ __launch_bounds__(128 * G) void k_attn_tile16(AttnParams a, float c) 
     // Double-buffered: block kb+1 is staged while block kb is computed.
     __shared__ __align__(16) uint16_t Ks_[2][kKeys * KS];
     __shared__ __align__(16) uint16_t Vs_[2][kKeys * VS];
-    __shared__ __align__(16) uint16_t tags_[2][kTileRows * TS];
+    // Score bias per (row, key) of a block: 0 for the row's entries, -inf
+    // elsewhere; it is the initial accumulator of the score product.  Three
+    // buffers: block kb+1's is written while block kb's is read, and block
+    // kb+2's is reset to -inf (its last reader was block kb-1, before the
+    // previous barrier).
+    __shared__ __align__(16) float bias_[3][kTileRows * BS];
     __shared__ int64_t rstart_s[kTileRows];
     __shared__ int32_t rlen_s[kTileRows];
     __shared__ int32_t any_s[2];
@@ -101,8 +113,8 @@ __global__ __launch_bounds__(128 * G) void k_attn_tile16(AttnParams a, float c) 
     const uint16_t* Vg = static_cast<const uint16_t*>(a.V) + (int64_t)g * N * D;
     if (!tile_is_dense(a, g, q0)) return;   // a sparse tile belongs to the gather kernel
 
-    // ---- per-row CSR extents, tags cleared
-    for (int i = tid; i < 2 * kTileRows * TS; i += NT) (&tags_[0][0])[i] = 0;
+    // ---- per-row CSR extents, bias buffers at -inf
+    for (int i = tid; i < 3 * kTileRows * BS; i += NT) (&bias_[0][0])[i] = -INFINITY;
     if (tid < 2) any_s[tid] = 0;
     if (tid < kTileRows) {
         const int64_t q = q0 + tid;
@@ -146,13 +158,17 @@ __global__ __launch_bounds__(128 * G) void k_attn_tile16(AttnParams a, float c) 
             qf[ks] = q < N ? v : zero;
         }
     }
-    float m_run = -INFINITY, l_run = 0.f;
+    float m_run = -INFINITY;   // reference max of this lane's query, log2 domain (scores x c)
     f32x4_t o[DT];
+    // Row sums of P on the matrix unit: an all-ones A operand makes every
+    // output row of lsum the sum over keys of this lane's query.
+    f32x4_t lsum = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    const u32x4_t ones = {0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u};
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) o[dt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     __syncthreads();
 
-    // Rows this wave turns into tags: r = w + NW*i.
+    // Rows whose bias this wave writes: r = w + NW*i.
     int64_t rst[RPW];
     int rln[RPW], cur[RPW];
 #pragma unroll
@@ -187,13 +203,12 @@ __global__ __launch_bounds__(128 * G) void k_attn_tile16(AttnParams a, float c) 
     };
 
     // Stage block kb (its K/V pieces are in kreg/vreg, its CSR windows in
-    // wreg) into LDS buffer p, with its tags; the "any entries" flag of the
+    // wreg) into LDS buffer p, with its bias; the "any entries" flag of the
     // buffer is stamped with kb + 1.
-    auto stage = [&](int kb, int p) {
+    auto stage = [&](int kb, int p, float* bias) {
         const int64_t k0 = (int64_t)kb * kKeys;
         uint16_t* Ks = Ks_[p];
         uint16_t* Vs = Vs_[p];
-        uint16_t* tags = tags_[p];
 #pragma unroll
         for (int u = 0; u < PPT; ++u) {
             const int e = tid + u * NT;
@@ -201,21 +216,23 @@ __global__ __launch_bounds__(128 * G) void k_attn_tile16(AttnParams a, float c) 
                 const int key = e / (D / 8), ch = e % (D / 8);
                 *reinterpret_cast<u32x4_t*>(&Ks[key * KS + ch * 8]) = kreg[u];   // rows past N: masked
                 u32x4_t v = vreg[u];
-                if (k0 + key >= N) v = u32x4_t{0u, 0u, 0u, 0u};   // V rows past N read as zeros
+                if (k0 + kKeys > N && k0 + key >= N) v = u32x4_t{0u, 0u, 0u, 0u};   // V rows past N read as zeros
                 *reinterpret_cast<u32x4_t*>(&Vs[key * VS + ch * 8]) = v;
             }
         }
-        const uint16_t tag = (uint16_t)(kb + 1);
+        const int k0i = kb * kKeys;
+        const uint32_t lim = (uint32_t)min(kKeys, (int)N - k0i);   // keys of the block inside [0, N)
         int my_cnt = 0;
 #pragma unroll
         for (int i = 0; i < RPW; ++i) {
             const int r = w + NW * i;
             if (r < kTileRows) {
-                const int col = wreg[i];
-                const int k0i = kb * kKeys;
-                const bool inb = col >= k0i && col < k0i + kKeys && col < (int)N;
+                // the window starts at the row's first unconsumed entry, so every
+                // valid entry is >= k0i; empty lanes hold -1
+                const uint32_t d = (uint32_t)(wreg[i] - k0i);
+                const bool inb = d < lim;
                 const uint64_t bal = __ballot(inb);
-                if (inb) tags[r * TS + (col - k0i)] = tag;
+                if (inb) bias[r * BS + d] = 0.f;
                 const int cnt = __popcll(bal);
                 cur[i] += cnt;
                 my_cnt += cnt;
@@ -227,7 +244,7 @@ __global__ __launch_bounds__(128 * G) void k_attn_tile16(AttnParams a, float c) 
     if (kb_lo <= kb_hi) {
         load_kv(kb_lo);
         load_windows();
-        stage(kb_lo, kb_lo & 1);
+        stage(kb_lo, kb_lo & 1, bias_[kb_lo % 3]);
         if (kb_lo < kb_hi) {
             load_kv(kb_lo + 1);
             load_windows();
@@ -237,10 +254,20 @@ __global__ __launch_bounds__(128 * G) void k_attn_tile16(AttnParams a, float c) 
     // One barrier per block: at iteration kb the workgroup stages block kb+1
     // into the other buffer (last read during iteration kb-1, before the
     // previous barrier) and computes block kb (staged before it).
+    int b3 = kb_lo % 3;                  // bias buffer of block kb
     for (int kb = kb_lo; kb <= kb_hi; ++kb) {
         const int p = kb & 1;
+        const int b3n = b3 == 2 ? 0 : b3 + 1, b3c = b3n == 2 ? 0 : b3n + 1;
+        {
+            // reset block kb+2's bias buffer
+            float* bc = bias_[b3c];
+            for (int e = tid; e < kTileRows * (kKeys / 4); e += NT) {
+                const int r = e / (kKeys / 4), c4 = e % (kKeys / 4);
+                *reinterpret_cast<f32x4_t*>(&bc[r * BS + 4 * c4]) = f32x4_t{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+            }
+        }
         if (kb < kb_hi) {
-            stage(kb + 1, p ^ 1);
+            stage(kb + 1, p ^ 1, bias_[b3n]);
             if (kb + 1 < kb_hi) {
                 load_kv(kb + 2);
                 load_windows();
@@ -248,15 +275,15 @@ __global__ __launch_bounds__(128 * G) void k_attn_tile16(AttnParams a, float c) 
         }
         const uint16_t* Ks = Ks_[p];
         const uint16_t* Vs = Vs_[p];
-        const uint16_t* tags = tags_[p];
-        const uint16_t tag = (uint16_t)(kb + 1);
+        const float* bias = bias_[b3];
+        b3 = b3n;
         const int any = any_s[p] == kb + 1;
         if (any) {
             // ---- S^T[key, query] = K_blk Q_h^T; st[kt][i] is key 16 kt + 4 (l/16) + i
             f32x4_t st[4];
 #pragma unroll
             for (int kt = 0; kt < 4; ++kt) {
-                st[kt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+                st[kt] = *reinterpret_cast<const f32x4_t*>(&bias[qr * BS + 16 * kt + 4 * lg]);
 #pragma unroll
                 for (int ks = 0; ks < KSL; ++ks) {
                     const u32x4_t av = *reinterpret_cast<const u32x4_t*>(&Ks[(16 * kt + li) * KS + 32 * ks + 8 * lg]);
@@ -267,36 +294,27 @@ __global__ __launch_bounds__(128 * G) void k_attn_tile16(AttnParams a, float c) 
             // ---- mask, one online-softmax step for this lane's query
             float mx = -INFINITY;
 #pragma unroll
-            for (int kt = 0; kt < 4; ++kt) {
-                const uint2 tg = *reinterpret_cast<const uint2*>(&tags[qr * TS + 16 * kt + 4 * lg]);
-                const uint32_t tv[4] = {tg.x & 0xFFFFu, tg.x >> 16, tg.y & 0xFFFFu, tg.y >> 16};
+            for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const float s = tv[i] == tag ? st[kt][i] : -INFINITY;
-                    st[kt][i] = s;
-                    mx = fmaxf(mx, s);
-                }
-            }
-            mx = quad_max16(mx);
-            const float m_new = fmaxf(m_run, mx);
-            const float m_use = m_new == -INFINITY ? 0.f : m_new;
-            const float mc = m_use * c;
-            float rs = 0.f;
+                for (int i = 0; i < 4; ++i) mx = fmaxf(mx, st[kt][i]);
+            // The reference max moves only when the block's max exceeds it by
+            // more than kSlack (log2 units): weights stay below 2^kSlack, and
+            // numerator and denominator share every rescale, so the result is
+            // the same up to rounding while rescales become rare.
+            const float mxc = quad_max16(mx) * c;
+            const bool move = mxc > m_run + kSlack;
+            const float m_new = move ? mxc : m_run;
+            const float mc = m_new == -INFINITY ? 0.f : m_new;
 #pragma unroll
             for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const float p = __builtin_amdgcn_exp2f(fmaf(st[kt][i], c, -mc));
-                    st[kt][i] = p;
-                    rs += p;
-                }
-            if (__ballot(m_new != m_run) != 0ull) {      // some query's max moved: rescale
-                const float corr = __builtin_amdgcn_exp2f(fmaf(m_run, c, -mc));
-                l_run *= corr;
+                for (int i = 0; i < 4; ++i) st[kt][i] = __builtin_amdgcn_exp2f(fmaf(st[kt][i], c, -mc));
+            if (__ballot(move) != 0ull) {
+                const float corr = __builtin_amdgcn_exp2f(m_run - mc);   // 0 on a query's first entries
+                lsum *= corr;
 #pragma unroll
                 for (int dt = 0; dt < DT; ++dt) o[dt] *= corr;
             }
-            l_run += rs;
             m_run = m_new;
             // ---- P^T as the B operand: 32-key step u holds keys 32u + 4 (l/16) + i
             // (slots 0..3) and 32u + 16 + 4 (l/16) + i (slots 4..7)
@@ -318,13 +336,14 @@ __global__ __launch_bounds__(128 * G) void k_attn_tile16(AttnParams a, float c) 
                     const u32x4_t av = {lo.x, lo.y, hi.x, hi.y};
                     o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(av), as_bf16x8(pb[u]), o[dt], 0, 0, 0);
                 }
+                lsum = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(ones), as_bf16x8(pb[u]), lsum, 0, 0, 0);
             }
         }
         __syncthreads();
     }
 
     // ---- normalise and store: o[dt][i] is dim 16 dt + 4 (l/16) + i of the query
-    l_run = quad_sum16(l_run);
+    const float l_run = lsum[0];
     const int64_t q = q0 + qr;
     if (q < N) {
         const float inv = l_run > 0.f ? 1.0f / l_run : 0.f;
