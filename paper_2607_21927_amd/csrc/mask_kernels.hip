@@ -64,18 +64,24 @@ __device__ __forceinline__ void split_draw(uint32_t idx, uint32_t draws, float i
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 // One lane's share of the batch's (seed, draw) pairs, OR-ed into the bitmap.
-// Each lane walks its draws one permutation step per iteration: a lane whose
-// value lands in the pool emits it and starts its next draw at once, so cycle
-// walks of different lengths do not hold the wave at the slowest lane.  Every
-// walk ends within the domain size (the cycle through j < n returns to j);
-// the step bound only makes that explicit.
+// Lane t takes the contiguous flat indices [t per, (t+1) per) (flat index =
+// seed * draws + draw), so its seed -- and the round keys it holds -- changes
+// at most a few times per batch.  Each lane walks its draws one permutation
+// step per iteration: a lane whose value lands in the pool emits it and starts
+// its next draw at once, so cycle walks of different lengths do not hold the
+// wave at the slowest lane.  Every walk returns to the pool within the domain
+// size (the cycle through j < n returns to j), so per * size iterations bound
+// the loop; the bound is a wave-uniform counter.
 template <int ROUNDS>
 __device__ __forceinline__ void walk_draws(const FeistelDomain& dom, const uint32_t* rks,
                                            uint32_t* bits, uint32_t total, uint32_t draws,
                                            float inv_draws) {
-    uint32_t idx = threadIdx.x;
-    uint32_t x = 0, steps = 0;
+    const uint32_t per = (total + kThreads - 1) / kThreads;
+    uint32_t idx = threadIdx.x * per;
+    const uint32_t end = min(idx + per, total);
+    if (idx >= end) return;
     int s = 0, j = 0;
+    split_draw(idx, draws, inv_draws, s, j);
     uint32_t w[kRowWords];
     auto load_words = [&]() {
         const u32x4_t w0 = *reinterpret_cast<const u32x4_t*>(&rks[s * kRowWords]);
@@ -83,36 +89,20 @@ __device__ __forceinline__ void walk_draws(const FeistelDomain& dom, const uint3
         w[0] = w0.x; w[1] = w0.y; w[2] = w0.z; w[3] = w0.w;
         w[4] = w1.x; w[5] = w1.y; w[6] = w1.z; w[7] = w1.w;
     };
-    // With at least kThreads draws per seed the next pair of a lane is its
-    // draw index plus kThreads, wrapping at most once into the next seed.
-    const bool incremental = draws >= (uint32_t)kThreads;
-    if (idx < total) {
-        split_draw(idx, draws, inv_draws, s, j);
-        x = (uint32_t)j;
-        load_words();
-    }
-    while (idx < total) {
+    load_words();
+    uint32_t x = (uint32_t)j;
+    const uint64_t max_it = (uint64_t)per * dom.size;
+    for (uint64_t it = 0; it < max_it; ++it) {
         x = feistel<ROUNDS>(x, w, dom.a, dom.b);
-        ++steps;
-        if (x < dom.n || steps >= dom.size) {
-            if (x >= dom.n) x = 0;
+        if (x < dom.n) {
             atomicOr(&bits[x >> 5], 1u << (x & 31u));
-            idx += kThreads;
-            steps = 0;
-            if (idx < total) {
-                if (incremental) {
-                    j += kThreads;
-                    if (j >= (int)draws) {
-                        j -= (int)draws;
-                        ++s;
-                        load_words();
-                    }
-                } else {
-                    split_draw(idx, draws, inv_draws, s, j);
-                    load_words();
-                }
-                x = (uint32_t)j;
+            if (++idx == end) break;
+            if (++j == (int)draws) {
+                j = 0;
+                ++s;
+                load_words();
             }
+            x = (uint32_t)j;
         }
     }
 }
