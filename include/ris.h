@@ -202,7 +202,7 @@ typedef struct {
     int32_t algo;            /* ris_attn_algo: GATHER = per-row gather kernel;  */
                              /* TILE = 32-row tiles on MFMA (bf16 only); AUTO  */
                              /* = per 32-row tile, TILE when the tile's union  */
-                             /* density is >= 6%, GATHER otherwise             */
+                             /* density is >= 6.8%, GATHER otherwise           */
 } ris_attn_desc;
 
 /*

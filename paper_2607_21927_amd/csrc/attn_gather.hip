@@ -1,19 +1,26 @@
-// Sparse attention, gather form: one wavefront per (kv_head g, query row q).
+// Sparse attention, gather form: one wavefront per (kv_head g, query row q),
+// for the 32-row tiles whose union density leaves the tiled kernel idle.
 //
-// The row's unified index set I(g, q) (CSR) is walked in chunks of 64 keys:
+// bf16 inputs (k_attn_gather16): the matrix unit does both products.  The
+// row's unified index set I(g, q) (CSR) is walked in 32-key tiles; each key
+// row of K and V is gathered once for all G query heads of the group (the
+// heads are the 16-wide MFMA dimension), one online softmax per head runs
+// over the whole set, and the next tile's rows are loaded while the current
+// one is computed.  Every index of the set enters the single normalisation
+// once (Pre-Fusion Unified Softmax; Methods, "Hybrid Anchor and Pre-Fusion
+// Unified Softmax").
+//
+// float32 inputs (k_attn_gather): vector-unit form.  Chunks of 64 keys:
 //   1. scores  -- lane l owns key j_l of the chunk, reads K[g, j_l] once and
 //      forms <Q[h, q], K[g, j_l]> for every query head h of the GQA group
-//      (the G query rows sit in LDS and are read as broadcasts), so one
-//      gather of the key row serves all G heads;
+//      (the G query rows sit in LDS and are read as broadcasts);
 //   2. softmax -- one running (max, sum) per head over the whole set:
 //      wavefront max and sum by DPP, rescale of the accumulators when the
-//      max grows.  Every index of the set enters this single normalisation
-//      once (Pre-Fusion Unified Softmax; Methods, "Hybrid Anchor and
-//      Pre-Fusion Unified Softmax");
+//      max grows;
 //   3. PV      -- lanes switch to owning D/64 consecutive dimensions; for each
 //      key of the chunk the wave reads the value row as one contiguous
 //      segment and accumulates p_h * V for all G heads.
-// Scores are kept in the log2 domain (scale * log2(e) folded into Q) so the
+// Scores are kept in the log2 domain (scale * log2(e) folded in) so the
 // exponentials are exp2.  Rows are launched in descending q: the heavy rows
 // start first.
 #include "ris_device.h"
@@ -69,8 +76,9 @@ __device__ __forceinline__ void load_dims(const void* base, int64_t off, float* 
     }
 }
 
-template <int D, bool BF16>
+template <int D>
 __global__ __launch_bounds__(64) void k_attn_gather(AttnParams a, float qscale) {
+    constexpr bool BF16 = false;                      // float32 inputs (bf16 runs on k_attn_gather16)
     constexpr int DPL = D / 64;                       // dims per lane in PV
     constexpr int VEC = BF16 ? 8 : 4;                 // elements per 16-byte load
     constexpr int NV = D / VEC;
@@ -215,18 +223,220 @@ __global__ __launch_bounds__(64) void k_attn_gather(AttnParams a, float qscale) 
     }
 }
 
+// ---------------------------------------------------------------------------
+// bf16 gather on the matrix unit: one wavefront per (kv_head g, query row q),
+// four rows per workgroup, no workgroup barriers (each wave owns a private
+// LDS slice).  The row's set is walked in 32-key tiles; the next tile's K and
+// V rows are loaded into registers before the current one is computed:
+//   * S^T = K Q^T on MFMA 16x16x32 bf16 with the G query heads of the group
+//     as the 16-wide dimension (K rows gathered straight from HBM into the
+//     A-operand layout: lane l loads key l%16 of a 16-key half, dims
+//     8 (l/16) + 32 s .. ), so one gather of a key row serves all G heads;
+//   * one online softmax per head (lane l owns head l%16; a head's running
+//     max and sum live in four lanes, combined with permlane swaps);
+//   * O += P V on MFMA with P packed to bf16 in registers and V staged
+//     row-major in the wave's LDS slice and read transposed.
+// ---------------------------------------------------------------------------
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+typedef short s16x4_t __attribute__((ext_vector_type(4)));
+
+constexpr int kGWaves = 4;            // rows (waves) per workgroup
+constexpr int kGTile = 32;            // keys per tile
+constexpr float kGNegBig = -1e30f;    // finite start of the running max
+
+__device__ __forceinline__ uint2 lds_read_tr16(const uint16_t* ptr) {
+    typedef __attribute__((address_space(3))) s16x4_t lds_s16x4;
+    const s16x4_t v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(ptr));
+    return __builtin_bit_cast(uint2, v);
+}
+__device__ __forceinline__ bf16x8_t as_bf16x8(u32x4_t v) { return __builtin_bit_cast(bf16x8_t, v); }
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+    const f32x2_t f = {lo, hi};
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(f, bf16x2_t));
+}
+
+template <int D>
+struct GTile {
+    u32x4_t k[2][D / 32];
+    u32x4_t v[2][D / 32];
+    uint32_t valid;       // bit 16 kb + i: key slot 16 kb + i is a real key
+};
+
+// Keys [v0, v0 + 32) of the row's CSR list (slot 16 kb + l%16 per lane).
+template <int D>
+__device__ __forceinline__ void gather_tile(const int32_t* idx, int64_t L, int64_t N, const uint16_t* Kg,
+                                            const uint16_t* Vg, int64_t v0, int li, int lg, GTile<D>& T) {
+    uint32_t vm = 0;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+        const int64_t v = v0 + 16 * kb + li;
+        int64_t j = v < L ? (int64_t)idx[v] : -1;
+        if (j >= N) j = -1;                            // an index outside [0, N) is ignored
+        vm |= (uint32_t)(__ballot(j >= 0) & 0xFFFFull) << (16 * kb);
+        const int64_t jj = j >= 0 ? j : 0;             // row 0 always exists
+        const uint16_t* kp = Kg + jj * D + 8 * lg;
+        const uint16_t* vp = Vg + jj * D + 8 * lg;
+#pragma unroll
+        for (int s = 0; s < D / 32; ++s) {
+            T.k[kb][s] = *reinterpret_cast<const u32x4_t*>(kp + 32 * s);
+            T.v[kb][s] = *reinterpret_cast<const u32x4_t*>(vp + 32 * s);
+        }
+    }
+    T.valid = vm;
+}
+
+template <int D>
+__global__ __launch_bounds__(64 * kGWaves, 2) void k_attn_gather16(AttnParams a, float c) {
+    constexpr int SL = D / 32;         // k-slices of the score product
+    constexpr int DB = D / 16;         // 16-dim blocks of the output
+    constexpr int VS = D + 16;         // V row stride in LDS (bf16 elements)
+    __shared__ __align__(16) uint16_t vlds[kGWaves * kGTile * VS];
+
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int li = lane & 15, lg = lane >> 4;
+    const int64_t N = a.N;
+    const int64_t f = (int64_t)blockIdx.x * kGWaves + wave;   // heavy rows first
+    if (f >= (int64_t)a.Hkv * N) return;
+    const int64_t q = N - 1 - f / a.Hkv;
+    const int g = (int)(f % a.Hkv);
+    if (tile_is_dense(a, g, q - q % kTileRows)) return;   // that tile runs on the tiled kernel
+    const int G = a.G;
+    uint16_t* vw = vlds + wave * kGTile * VS;
+    const int64_t start = a.row_ptr[(int64_t)g * N + q];
+    const int64_t L = a.row_ptr[(int64_t)g * N + q + 1] - start;
+    const int32_t* idx = a.col_idx + start;
+    const uint16_t* Kg = static_cast<const uint16_t*>(a.K) + (int64_t)g * N * D;
+    const uint16_t* Vg = static_cast<const uint16_t*>(a.V) + (int64_t)g * N * D;
+
+    // ---- Q^T as the B operand: lane l holds head l%16, dims 32 s + 8 (l/16) ..
+    u32x4_t qf[SL];
+    {
+        const bool hv = li < G;
+        const uint16_t* qp = static_cast<const uint16_t*>(a.Q) + ((int64_t)(g * G + (hv ? li : 0)) * N + q) * D + 8 * lg;
+        const u32x4_t zero = {0u, 0u, 0u, 0u};
+#pragma unroll
+        for (int s = 0; s < SL; ++s) {
+            const u32x4_t v = *reinterpret_cast<const u32x4_t*>(qp + 32 * s);
+            qf[s] = hv ? v : zero;
+        }
+    }
+    f32x4_t o[DB];
+#pragma unroll
+    for (int db = 0; db < DB; ++db) o[db] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    float m_run = kGNegBig, l_run = 0.f;
+
+    if (L > 0) {
+        GTile<D> cur;
+        gather_tile<D>(idx, L, N, Kg, Vg, 0, li, lg, cur);
+        for (int64_t v0 = 0; v0 < L; v0 += kGTile) {
+            GTile<D> nxt;
+            const bool more = v0 + kGTile < L;
+            if (more) gather_tile<D>(idx, L, N, Kg, Vg, v0 + kGTile, li, lg, nxt);
+
+            // V rows into this wave's LDS slice, row-major (key slot 16 kb + l%16)
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                for (int s = 0; s < SL; ++s)
+                    *reinterpret_cast<u32x4_t*>(vw + (16 * kb + li) * VS + 32 * s + 8 * lg) = cur.v[kb][s];
+
+            // S^T = K Q^T: lane l holds head l%16 at key slots 16 kb + 4 (l/16) + i
+            f32x4_t st[2];
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb) {
+                st[kb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int s = 0; s < SL; ++s)
+                    st[kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(cur.k[kb][s]), as_bf16x8(qf[s]),
+                                                                      st[kb], 0, 0, 0);
+            }
+            // online softmax over the tile (scores in the log2 domain)
+            float sc[2][4];
+            float mx = -INFINITY;
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const bool ok = (cur.valid >> (16 * kb + 4 * lg + i)) & 1u;
+                    sc[kb][i] = ok ? st[kb][i] * c : -INFINITY;
+                    mx = fmaxf(mx, sc[kb][i]);
+                }
+            mx = quad_max16(mx);
+            const float m_new = fmaxf(m_run, mx);
+            const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+            float pv[2][4];
+            float ps = 0.f;
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    pv[kb][i] = __builtin_amdgcn_exp2f(sc[kb][i] - m_new);
+                    ps += pv[kb][i];
+                }
+            l_run = l_run * alpha + ps;
+            m_run = m_new;
+            // rescale the output rows: lane l holds heads 4 (l/16) + i
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const float al = __shfl(alpha, 4 * lg + i);
+#pragma unroll
+                for (int db = 0; db < DB; ++db) o[db][i] *= al;
+            }
+            // P as the A operand (head l%16; k slots 8 (l/16) + e hold keys
+            // 4 (l/16) + e and 16 + 4 (l/16) + e - 4); V as the B operand in
+            // the same key order via the transpose read
+            const u32x4_t pk = {pack_bf16x2(pv[0][0], pv[0][1]), pack_bf16x2(pv[0][2], pv[0][3]),
+                                pack_bf16x2(pv[1][0], pv[1][1]), pack_bf16x2(pv[1][2], pv[1][3])};
+            const uint16_t* v_lo = vw + (lane >> 2) * VS + 4 * (lane & 3);
+            const uint16_t* v_hi = v_lo + 16 * VS;
+#pragma unroll
+            for (int db = 0; db < DB; ++db) {
+                const uint2 x = lds_read_tr16(v_lo + 16 * db);
+                const uint2 y = lds_read_tr16(v_hi + 16 * db);
+                const u32x4_t vb = {x.x, x.y, y.x, y.y};
+                o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(pk), as_bf16x8(vb), o[db], 0, 0, 0);
+            }
+            if (more) cur = nxt;
+        }
+    }
+
+    // ---- normalise and store: o[db][i] is dim 16 db + l%16 of head 4 (l/16) + i
+    l_run = quad_sum16(l_run);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int h = 4 * lg + i;
+        const float lh = __shfl(l_run, h);
+        if (h < G) {
+            const float inv = lh > 0.f ? 1.0f / lh : 0.f;
+            const int64_t base = ((int64_t)(g * G + h) * N + q) * D + li;
+#pragma unroll
+            for (int db = 0; db < DB; ++db) {
+                const float val = o[db][i] * inv;
+                if (a.out_bf16) static_cast<uint16_t*>(a.out)[base + 16 * db] = f32_to_bf16(val);
+                else static_cast<float*>(a.out)[base + 16 * db] = val;
+            }
+        }
+    }
+}
+
 }  // namespace
 
 hipError_t launch_attn_gather(const AttnParams& a, hipStream_t st) {
     const float qscale = a.scale * 1.4426950408889634f;   // log2(e): scores in log2 domain
-    const dim3 grid((unsigned)((int64_t)a.Hkv * a.N)), block(64);
-    if (a.D == 128) {
-        if (a.in_bf16) hipLaunchKernelGGL((k_attn_gather<128, true>), grid, block, 0, st, a, qscale);
-        else hipLaunchKernelGGL((k_attn_gather<128, false>), grid, block, 0, st, a, qscale);
-    } else {
-        if (a.in_bf16) hipLaunchKernelGGL((k_attn_gather<64, true>), grid, block, 0, st, a, qscale);
-        else hipLaunchKernelGGL((k_attn_gather<64, false>), grid, block, 0, st, a, qscale);
+    if (a.in_bf16) {
+        const int64_t rows = (int64_t)a.Hkv * a.N;
+        const dim3 grid((unsigned)((rows + kGWaves - 1) / kGWaves)), block(64 * kGWaves);
+        if (a.D == 128) hipLaunchKernelGGL((k_attn_gather16<128>), grid, block, 0, st, a, qscale);
+        else hipLaunchKernelGGL((k_attn_gather16<64>), grid, block, 0, st, a, qscale);
+        return hipGetLastError();
     }
+    const dim3 grid((unsigned)((int64_t)a.Hkv * a.N)), block(64);
+    if (a.D == 128) hipLaunchKernelGGL((k_attn_gather<128>), grid, block, 0, st, a, qscale);
+    else hipLaunchKernelGGL((k_attn_gather<64>), grid, block, 0, st, a, qscale);
     return hipGetLastError();
 }
 

@@ -1,12 +1,13 @@
 """GPU sparse attention (ris_sparse_attn) vs the oracle.
 
 Bars: max |out - oracle| <= 1e-5 for float32 inputs and <= 2e-2 for bf16
-inputs with float32 accumulation.  Tighter bars derived from each kernel's
-arithmetic are asserted as well, to catch errors the loose bar would hide:
-the gather kernel forms exact bf16 products and sums in float32 (2e-4); the
-tiled kernel also rounds the softmax weights to bf16 before the PV matrix
-product, a relative perturbation of at most 2^-9 per weight, so its outputs
-move by at most 2^-9 max|V| (max|V| < 5.5 for every input used here).
+inputs with float32 accumulation.  A tighter bar derived from the kernels'
+arithmetic is asserted as well, to catch errors the loose bar would hide:
+for bf16 inputs both kernels (gather and tiled) form exact bf16 products
+with float32 sums and round the softmax weights to bf16 before the PV
+matrix product, a relative perturbation of at most 2^-9 per weight, so the
+outputs move by at most 2^-9 max|V| + 2e-4 (max|V| < 5.5 for every input
+used here).
 Both sides read the same seeded inputs and use their own index sets (the
 GPU's CSR from ris_mask_build, the oracle's from its own definition).
 """
@@ -46,9 +47,9 @@ def run_case(Hq, Hkv, N, D, mode, ppm, S, block=0, dtype_in="bf16", dtype_out="f
 
 
 def tight_tol(algo, V_max):
-    """Derived bound: gather 2e-4; tiled (and AUTO, which may use it) adds
-    the bf16 rounding of the softmax weights, 2^-9 max|V|."""
-    return 2e-4 if algo == 1 else 2.0**-9 * V_max + 2e-4
+    """Derived bound for bf16 inputs (every algorithm): float32 sums of exact
+    products, plus the bf16 rounding of the softmax weights, 2^-9 max|V|."""
+    return 2.0**-9 * V_max + 2e-4
 
 
 CASES = [
@@ -151,7 +152,7 @@ def test_auto_dispatch_mixed_density():
     assert float(np.abs(got - want).max()) <= tight_tol(0, 5.5)
     got_g, _, _ = run_case(12, 2, N, 128, 0, ppm, S, algo=1)
     got_t, _, _ = run_case(12, 2, N, 128, 0, ppm, S, algo=2)
-    tau = float(np.float32(0.06))            # the library's threshold, as float32
+    tau = float(np.float32(0.068))           # the library's threshold, as float32
     sp = spec_of(0, ppm, N, 2, S)
     dense = np.zeros(N, dtype=bool)
     for q0 in range(0, N, 32):
