@@ -195,6 +195,40 @@ def run_gpu(w, layers, Q, K, V, steps, warmup, algo):
                 ms_attn=t_attn / steps, nnz=sum(nnz), layers=len(descs))
 
 
+def kv_gather_figure(w, reps=5):
+    """The gather kernel on the workload's own shape and density with a single
+    seed (the union then stays below the tiled kernel's threshold, so every
+    row takes the per-row K/V gather): algorithmic K/V bytes per second."""
+    import torch
+    from paper_2607_21927_amd import ris
+    dev = torch.device("cuda:0")
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(1)
+    q = torch.randn(w.Hq, w.N, w.D, generator=gen, device=dev).to(torch.bfloat16)
+    k = torch.randn(w.Hkv, w.N, w.D, generator=gen, device=dev).to(torch.bfloat16)
+    v = torch.randn(w.Hkv, w.N, w.D, generator=gen, device=dev).to(torch.bfloat16)
+    d = ris.mask_desc(w.mode, w.density_ppm, w.N, w.Hkv, n_seeds=1, seed=w.seed, block=w.block)
+    rp, ci = ris.build_csr(d, dev, use_bound=True)
+    nnz = int(rp[-1].item())
+    out = torch.empty_like(q)
+    ad = ris.attn_desc(q, k, out, mode=w.mode, block=w.block, algo=ris.ATTN_GATHER)
+    for _ in range(2):
+        ris.sparse_attn(q, k, v, rp, ci, out, ad)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        ris.sparse_attn(q, k, v, rp, ci, out, ad)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    achieved = nnz * KV_PAIR_BYTES[w.D] / (ms * 1e-3) / 1e9
+    return {"kernel": f"k_attn_gather16<{w.D}>", "seeds": 1,
+            "union_fraction": nnz / (w.Hkv * w.N * (w.N + 1) / 2), "kv_pairs": nnz, "ms": ms,
+            "achieved": achieved, "unit": "GB/s", "peak": HBM_PEAK_GBS, "frac": achieved / HBM_PEAK_GBS,
+            "bytes_per_kv_pair": KV_PAIR_BYTES[w.D]}
+
+
 def measured_traffic(workload, kernel_source):
     """HBM bytes per launch of the attention kernel from the committed
     rocprofv3 counter record, or None when no record exists for this
@@ -453,6 +487,8 @@ def main():
     ap.add_argument("--model", choices=sorted(MODEL_WORKLOAD),
                     help="time a model-level prefill of the named random-weight stack")
     ap.add_argument("--model-layers", type=int, default=0, help="layers of the stack (0 = all)")
+    ap.add_argument("--kv-gather", action="store_true",
+                    help="time only the per-row K/V gather kernel (workload shape, one seed)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: the hot path needs no cross-GPU exchange and this "
@@ -460,6 +496,21 @@ def main():
         sys.exit(2)
     if args.model:
         print(json.dumps(run_model_bench(args.model, args.model_layers, args.steps, args.warmup)))
+        return
+    if args.kv_gather:
+        w = WORKLOADS[args.workload]
+        f = kv_gather_figure(w, reps=args.steps)
+        print(json.dumps({"metric": "K/V gather bandwidth (algorithmic bytes / kernel time)",
+                          "value": f["achieved"], "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
+                          "warmup": 2, "ms_per_step": f["ms"], "higher_is_better": True,
+                          "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+                          "data": "synthetic: Gaussian Q/K/V (torch.randn, seed 1)",
+                          "config": {"workload": w.name + "_1seed", "N": w.N, "Hq": w.Hq, "Hkv": w.Hkv,
+                                     "head_dim": w.D, "density": w.density_ppm / 1e6, "seeds": 1},
+                          "roofline": {"bound": "hbm", "achieved": f["achieved"], "peak": HBM_PEAK_GBS,
+                                       "unit": "GB/s", "frac": f["frac"], "traffic": None,
+                                       "kernel": f["kernel"], "bytes_per_kv_pair": f["bytes_per_kv_pair"]},
+                          "kv_pairs": f["kv_pairs"], "union_fraction": f["union_fraction"]}))
         return
     if args.decode:
         wl = args.workload if args.workload != "qwen2_64k_stochastic_yarn" else "qwen2_64k_full_geometry"
@@ -487,6 +538,7 @@ def main():
     achieved = alg_bytes / (g["ms_attn"] * 1e-3) / 1e9
     tiled = w.dtype == "bf16" and args.algo != 1
     traffic = measured_traffic(w.name, "paper_2607_21927_amd/csrc/attn_tile.hip") if tiled else None
+    gather = kv_gather_figure(w) if w.dtype == "bf16" and not args.all_layers else None
     res = {
         "metric": "attended (q,k) pairs/s (whole hot-path step: RoPE + geometry + attention)",
         "value": pairs / (g["ms_step"] * 1e-3),
@@ -516,7 +568,8 @@ def main():
         "hbm_gbs_attn": achieved,
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
-                     "kernel": f"k_attn_tile16<{w.D}, {G}>" if tiled else f"k_attn_gather<{w.D}>",
+                     "kernel": (f"k_attn_tile16<{w.D}, {G}>" if tiled else
+                                f"k_attn_gather16<{w.D}>" if w.dtype == "bf16" else f"k_attn_gather<{w.D}>"),
                      "measured_copy_gbs": g["copy_gbs"], "frac_of_measured_copy": achieved / g["copy_gbs"],
                      "bytes_per_kv_pair": KV_PAIR_BYTES[w.D]},
         # The tiled kernel reads each K/V block once per 32 rows, so its real
@@ -529,6 +582,8 @@ def main():
             "frac": pairs * 4 * w.D / (g["ms_attn"] * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFS,
             "issued_dense_masked_tflops": (w.Hq * causal_pairs / w.Hkv * 4 * w.D
                                            / (g["ms_attn"] * 1e-3) / 1e12) if tiled else None},
+        # The per-row K/V gather path (sparse unions), on this shape with one seed.
+        "kv_gather": gather,
         "cpu_baseline": cpu,
     }
     print(json.dumps(res))
