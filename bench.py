@@ -489,6 +489,8 @@ def main():
     ap.add_argument("--model-layers", type=int, default=0, help="layers of the stack (0 = all)")
     ap.add_argument("--kv-gather", action="store_true",
                     help="time only the per-row K/V gather kernel (workload shape, one seed)")
+    ap.add_argument("--no-kv-gather", action="store_true",
+                    help="leave the K/V gather figure out of the default line (profiling runs)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: the hot path needs no cross-GPU exchange and this "
@@ -538,7 +540,8 @@ def main():
     achieved = alg_bytes / (g["ms_attn"] * 1e-3) / 1e9
     tiled = w.dtype == "bf16" and args.algo != 1
     traffic = measured_traffic(w.name, "paper_2607_21927_amd/csrc/attn_tile.hip") if tiled else None
-    gather = kv_gather_figure(w) if w.dtype == "bf16" and not args.all_layers else None
+    gather = (kv_gather_figure(w) if w.dtype == "bf16" and not args.all_layers and not args.no_kv_gather
+              else None)
     res = {
         "metric": "attended (q,k) pairs/s (whole hot-path step: RoPE + geometry + attention)",
         "value": pairs / (g["ms_step"] * 1e-3),
