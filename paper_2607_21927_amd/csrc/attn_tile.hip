@@ -95,7 +95,6 @@ __global__ __launch_bounds__(128 * G) void k_attn_tile16(AttnParams a, float c) 
     __shared__ __align__(16) float bias_[3][kTileRows * BS];
     __shared__ int64_t rstart_s[kTileRows];
     __shared__ int32_t rlen_s[kTileRows];
-    __shared__ int32_t any_s[2];
     __shared__ int32_t kb_range[2];
 
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -115,7 +114,6 @@ __global__ __launch_bounds__(128 * G) void k_attn_tile16(AttnParams a, float c) 
 
     // ---- per-row CSR extents, bias buffers at -inf
     for (int i = tid; i < 3 * kTileRows * BS; i += NT) (&bias_[0][0])[i] = -INFINITY;
-    if (tid < 2) any_s[tid] = 0;
     if (tid < kTileRows) {
         const int64_t q = q0 + tid;
         int64_t s = 0, L = 0;
@@ -203,8 +201,7 @@ __global__ __launch_bounds__(128 * G) void k_attn_tile16(AttnParams a, float c) 
     };
 
     // Stage block kb (its K/V pieces are in kreg/vreg, its CSR windows in
-    // wreg) into LDS buffer p, with its bias; the "any entries" flag of the
-    // buffer is stamped with kb + 1.
+    // wreg) into LDS buffer p, with its bias.
     auto stage = [&](int kb, int p, float* bias) {
         const int64_t k0 = (int64_t)kb * kKeys;
         uint16_t* Ks = Ks_[p];
@@ -222,7 +219,6 @@ __global__ __launch_bounds__(128 * G) void k_attn_tile16(AttnParams a, float c) 
         }
         const int k0i = kb * kKeys;
         const uint32_t lim = (uint32_t)min(kKeys, (int)N - k0i);   // keys of the block inside [0, N)
-        int my_cnt = 0;
 #pragma unroll
         for (int i = 0; i < RPW; ++i) {
             const int r = w + NW * i;
@@ -233,12 +229,9 @@ __global__ __launch_bounds__(128 * G) void k_attn_tile16(AttnParams a, float c) 
                 const bool inb = d < lim;
                 const uint64_t bal = __ballot(inb);
                 if (inb) bias[r * BS + d] = 0.f;
-                const int cnt = __popcll(bal);
-                cur[i] += cnt;
-                my_cnt += cnt;
+                cur[i] += __popcll(bal);
             }
         }
-        if (lane == 0 && my_cnt) any_s[p] = kb + 1;
     };
 
     if (kb_lo <= kb_hi) {
@@ -277,8 +270,10 @@ __global__ __launch_bounds__(128 * G) void k_attn_tile16(AttnParams a, float c) 
         const uint16_t* Vs = Vs_[p];
         const float* bias = bias_[b3];
         b3 = b3n;
-        const int any = any_s[p] == kb + 1;
-        if (any) {
+        {
+            // Every block of the range is computed: at the union densities the
+            // tiled kernel takes, a 64-key block with no entry in any of the
+            // 32 rows is rare, and a fully masked block adds exact zeros.
             // ---- S^T[key, query] = K_blk Q_h^T; st[kt][i] is key 16 kt + 4 (l/16) + i
             f32x4_t st[4];
 #pragma unroll
