@@ -182,6 +182,55 @@ __device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* r
     return before + inc - v;
 }
 
+// Write the row: the set bits of bits[0, W) as keys 32 w + b, ascending, at
+// out[0, ..), then the Structural clique; nothing at out[limit] or beyond.
+// A lane's keys of one word are contiguous in out, so it writes them four at
+// a time with 16-byte stores once its position is 16-byte aligned (scalar
+// stores at the two ends): a quarter of the store instructions of one key
+// per store.
+__device__ void emit_row(const uint32_t* bits, uint32_t W, int32_t* out, int64_t limit, const RowGeom& g,
+                         uint32_t* red) {
+    uint32_t done = 0;
+    for (uint32_t w0 = 0; w0 < W; w0 += kThreads) {
+        const uint32_t w = w0 + threadIdx.x;
+        uint32_t word = w < W ? bits[w] : 0u;
+        uint32_t total;
+        int64_t pos = done + block_exclusive_scan(__popc(word), red, &total);
+        const int32_t k0 = (int32_t)(w * 32u);
+        auto next_key = [&]() {
+            const uint32_t b = __ffs(word) - 1u;
+            word &= word - 1u;
+            return k0 + (int32_t)b;
+        };
+        while (word && (reinterpret_cast<uintptr_t>(out + pos) & 15u)) {
+            const int32_t k = next_key();
+            if (pos < limit) out[pos] = k;
+            ++pos;
+        }
+        while (__popc(word) >= 4) {
+            const int32_t a = next_key(), b = next_key(), c = next_key(), d = next_key();
+            if (pos + 4 <= limit) {
+                *reinterpret_cast<int4*>(out + pos) = make_int4(a, b, c, d);
+            } else {
+                if (pos < limit) out[pos] = a;
+                if (pos + 1 < limit) out[pos + 1] = b;
+                if (pos + 2 < limit) out[pos + 2] = c;
+            }
+            pos += 4;
+        }
+        while (word) {
+            const int32_t k = next_key();
+            if (pos < limit) out[pos] = k;
+            ++pos;
+        }
+        done += total;
+    }
+    for (uint32_t t = threadIdx.x; t < g.clique_len; t += kThreads) {
+        const int64_t pos = (int64_t)done + t;
+        if (pos < limit) out[pos] = (int32_t)(g.clique_start + t);
+    }
+}
+
 // Workgroup -> (row r, query q, head h), heavy (late) rows first.
 __device__ __forceinline__ void row_of_block(const MaskParams& p, int64_t& r, int64_t& q, int& h) {
     const int64_t i = blockIdx.x;
@@ -224,24 +273,7 @@ __global__ __launch_bounds__(kThreads) void k_mask_fill(MaskParams p, const int6
     build_row_bitmap(p, q, h, g, rks, bits);
     const uint32_t W = (g.pool + 31u) >> 5;
     int32_t* out = col_idx + base;
-    uint32_t done = 0;
-    for (uint32_t w0 = 0; w0 < W; w0 += kThreads) {
-        const uint32_t w = w0 + threadIdx.x;
-        uint32_t word = w < W ? bits[w] : 0u;
-        uint32_t total;
-        int64_t pos = done + block_exclusive_scan(__popc(word), red, &total);
-        while (word) {
-            const uint32_t b = __ffs(word) - 1u;
-            word &= word - 1u;
-            if (pos < limit) out[pos] = (int32_t)(w * 32u + b);
-            ++pos;
-        }
-        done += total;
-    }
-    for (uint32_t t = threadIdx.x; t < g.clique_len; t += kThreads) {
-        const int64_t pos = (int64_t)done + t;
-        if (pos < limit) out[pos] = (int32_t)(g.clique_start + t);
-    }
+    emit_row(bits, W, out, limit, g, red);
 }
 
 // ---------------------------------------------------------------------------
@@ -331,24 +363,7 @@ __global__ __launch_bounds__(kThreads) void k_mask_fused(MaskParams p, int64_t* 
     int64_t limit = count;
     if (limit > capacity - base) limit = capacity - base;
     int32_t* out = col_idx + base;
-    uint32_t done = 0;
-    for (uint32_t w0 = 0; w0 < W; w0 += kThreads) {
-        const uint32_t w = w0 + threadIdx.x;
-        uint32_t word = w < W ? bits[w] : 0u;
-        uint32_t total;
-        int64_t pos = done + block_exclusive_scan(__popc(word), red, &total);
-        while (word) {
-            const uint32_t b = __ffs(word) - 1u;
-            word &= word - 1u;
-            if (pos < limit) out[pos] = (int32_t)(w * 32u + b);
-            ++pos;
-        }
-        done += total;
-    }
-    for (uint32_t t = threadIdx.x; t < g.clique_len; t += kThreads) {
-        const int64_t pos = (int64_t)done + t;
-        if (pos < limit) out[pos] = (int32_t)(g.clique_start + t);
-    }
+    emit_row(bits, W, out, limit, g, red);
 }
 
 __global__ void k_fill_i64(int64_t* x, int64_t n, int64_t v) {

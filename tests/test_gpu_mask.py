@@ -61,6 +61,33 @@ def test_mask_bound_sized_fill_and_determinism():
     assert torch.equal(rp2, rp3) and torch.equal(ci2, ci3)
 
 
+@pytest.mark.parametrize("shift", [1, 2, 3])
+def test_mask_into_unaligned_buffer(shift):
+    """col_idx starting 1-3 elements past a 16-byte boundary: the rows are
+    written with scalar stores up to the first aligned position and 16-byte
+    stores after it; every element, and nothing around the written range,
+    must come out as from an aligned buffer (one pass and two phases)."""
+    ris = need_gpu()
+    sp = spec_of(0, 200_000, 1500, 2, 6)
+    d = desc_of(ris, sp)
+    rp, ci = gpu_csr(ris, sp)
+    nnz = int(rp[-1].item())
+    cap = ris.mask_nnz_bound(d)
+    for use_bound in (True, False):
+        base = torch.full((cap + 8,), -5, dtype=torch.int32, device="cuda")
+        view = base[shift:shift + (cap if use_bound else nnz)]
+        rp2 = torch.empty_like(rp)
+        if use_bound:
+            ris.mask_build(d, rp2, view, col_capacity=cap)
+        else:
+            ris.mask_build(d, rp2)
+            ris.mask_build(d, rp2, view)
+        torch.cuda.synchronize()
+        assert torch.equal(rp2, rp)
+        assert torch.equal(view[:nnz], ci[:nnz])
+        assert bool((base[:shift] == -5).all()) and bool((base[shift + nnz:] == -5).all())
+
+
 def test_mask_capacity_error_writes_nothing():
     ris = need_gpu()
     sp = spec_of(0, 50_000, 2000, 2, 5)
