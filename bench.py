@@ -128,7 +128,9 @@ def run_gpu(w, layers, Q, K, V, steps, warmup, algo):
         # Needles are planted on rotated vectors; this workload's step then
         # starts from the rotated, planted inputs and skips RoPE.
         raise SystemExit("needle workload: run its parity test instead")
-    q, k = torch.empty_like(q0), torch.empty_like(k0)
+    # RoPE reads the unrotated inputs and writes the rotated Q and K (the
+    # inputs stay as they are, so every step starts from the same data).
+    q, k = (torch.empty_like(q0), torch.empty_like(k0)) if w.rope != ROPE_NONE else (q0, k0)
     out = torch.empty(w.Hq, w.N, w.D, dtype=torch.bfloat16, device=dev)
     descs = [ris.mask_desc(w.mode, w.density_ppm, w.N, w.Hkv, n_seeds=w.n_seeds, seed=w.seed,
                            layer=layer, block=w.block, window=w.window, anchor=w.anchor)
@@ -147,13 +149,11 @@ def run_gpu(w, layers, Q, K, V, steps, warmup, algo):
         # geometry (the layer index enters the hash) over the same inputs.
         for i, desc in enumerate(descs):
             ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)] if stamps is not None else None
-            q.copy_(q0)
-            k.copy_(k0)
             if ev:
                 ev[0].record()
             if rd is not None:
-                ris.rope(q, rd)
-                ris.rope(k, rd)
+                ris.rope_from(q0, q, rd)
+                ris.rope_from(k0, k, rd)
             if ev:
                 ev[1].record()
             # col_idx sized from the closed-form bound: one call builds the CSR.

@@ -184,6 +184,20 @@ typedef struct {
 int ris_rope(void* x, int32_t dtype, int32_t heads, int64_t N, int32_t D, int64_t pos0,
              const ris_rope_desc* desc, void* stream);
 
+/*
+ * The same rotation read from a strided source and written to x, device
+ * [heads, N, D] contiguous: element (h, t, d) of the source is at src +
+ * h * head_stride + t * token_stride + d (strides in elements, >= 0, of the
+ * same dtype).  src is only read.  x may be src itself with head_stride =
+ * N * D and token_stride = D (that is ris_rope); any other overlap of the two
+ * ranges is undefined.  Serves out-of-place rotation and, with head_stride =
+ * D and token_stride = the row length of a token-major projection output,
+ * the head-major layout and the rotation in one pass.
+ */
+int ris_rope_from(const void* src, int64_t head_stride, int64_t token_stride, void* x, int32_t dtype,
+                  int32_t heads, int64_t N, int32_t D, int64_t pos0, const ris_rope_desc* desc,
+                  void* stream);
+
 /* ------------------------------------------------------------------------ */
 /* Sparse attention over the unified index sets                             */
 /* ------------------------------------------------------------------------ */
@@ -299,7 +313,8 @@ const char* ris_status_string(int status);
 
 /* Library ABI version: (major << 16) | minor.  2.0 added window and anchor to
  * ris_mask_desc; 2.1 added the row-range build and the decode step; 2.2 the
- * host-model layers (RMSNorm, SwiGLU). */
+ * host-model layers (RMSNorm, SwiGLU); 2.3 the strided rotation
+ * ris_rope_from. */
 int ris_version(void);
 
 #ifdef __cplusplus

@@ -100,7 +100,7 @@ constexpr float kAutoDensity = 0.068f;
 
 extern "C" {
 
-int ris_version(void) { return (2 << 16) | 2; }
+int ris_version(void) { return (2 << 16) | 3; }
 
 const char* ris_status_string(int status) {
     switch (status) {
@@ -157,7 +157,13 @@ int ris_mask_build(const ris_mask_desc* desc, int64_t* row_ptr, int32_t* col_idx
 
 int ris_rope(void* x, int32_t dtype, int32_t heads, int64_t N, int32_t D, int64_t pos0,
              const ris_rope_desc* desc, void* stream) {
-    if (!x || !desc) return RIS_E_ARG;
+    return ris_rope_from(x, N * D, D, x, dtype, heads, N, D, pos0, desc, stream);
+}
+
+int ris_rope_from(const void* src, int64_t head_stride, int64_t token_stride, void* x, int32_t dtype,
+                  int32_t heads, int64_t N, int32_t D, int64_t pos0, const ris_rope_desc* desc, void* stream) {
+    if (!src || !x || !desc) return RIS_E_ARG;
+    if (head_stride < 0 || token_stride < 0) return RIS_E_ARG;
     if (dtype != RIS_F32 && dtype != RIS_BF16) return RIS_E_DTYPE;
     if (heads < 1 || N < 1 || pos0 < 0) return RIS_E_ARG;
     if (D < 2 || (D & 1) || D / 2 > ris::kMaxRopeHalf) return RIS_E_SHAPE;
@@ -199,8 +205,8 @@ int ris_rope(void* x, int32_t dtype, int32_t heads, int64_t N, int32_t D, int64_
         tab.inv_freq[i] = f;
     }
     tab.mscale = (desc->kind == RIS_ROPE_YARN && s > 1.0) ? 0.1 * log(s) + 1.0 : 1.0;
-    return hip_status(ris::launch_rope(x, dtype == RIS_BF16, heads, N, D, pos0, tab,
-                                       static_cast<hipStream_t>(stream)));
+    return hip_status(ris::launch_rope(src, head_stride, token_stride, x, dtype == RIS_BF16, heads, N, D, pos0,
+                                       tab, static_cast<hipStream_t>(stream)));
 }
 
 int ris_sparse_attn(const void* Q, const void* K, const void* V, const int64_t* row_ptr,

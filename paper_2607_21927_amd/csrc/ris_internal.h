@@ -34,8 +34,8 @@ struct RopeTable {
     double inv_freq[kMaxRopeHalf];
     double mscale;
 };
-hipError_t launch_rope(void* x, int dtype_bf16, int heads, int64_t N, int D, int64_t pos0,
-                       const RopeTable& tab, hipStream_t st);
+hipError_t launch_rope(const void* src, int64_t head_stride, int64_t token_stride, void* dst, int dtype_bf16,
+                       int heads, int64_t N, int D, int64_t pos0, const RopeTable& tab, hipStream_t st);
 
 struct AttnParams {
     const void* Q;

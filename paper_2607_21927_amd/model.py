@@ -5,8 +5,9 @@ The paper replaces only the attention of the host model and leaves its
 weights and every other layer as they are (Methods, opening of "The RIS
 Implementation").  Per layer:
 
-    ris_rmsnorm (fused residual add) -> QKV GEMM -> head-major Q, K, V
-    -> ris_rope on Q and K -> ris_mask_build (this layer's geometry)
+    ris_rmsnorm (fused residual add) -> QKV GEMM -> head-major V
+    -> ris_rope_from on Q and K (head-major layout and rotation in one pass)
+    -> ris_mask_build (this layer's geometry)
     -> ris_sparse_attn -> O GEMM -> ris_rmsnorm (fused residual add)
     -> gate/up GEMM -> ris_swiglu -> down GEMM
 
@@ -68,14 +69,18 @@ class PrefillModel:
             qkv = torch.addmm(layer["bqkv"], h, layer["wqkv_t"])
         else:
             qkv = torch.mm(h, layer["wqkv_t"])
-        q = qkv[:, :Hq * D].view(N, Hq, D).transpose(0, 1).contiguous()
-        k = qkv[:, Hq * D:(Hq + Hkv) * D].view(N, Hkv, D).transpose(0, 1).contiguous()
         v = qkv[:, (Hq + Hkv) * D:].view(N, Hkv, D).transpose(0, 1).contiguous()
         if timers:
             timers.mark("proj")
+        # Q and K: head-major layout and rotation in one pass over the
+        # projection output (ris_rope_from reads the strided head columns).
+        qv = qkv[:, :Hq * D].view(N, Hq, D).transpose(0, 1)
+        kv = qkv[:, Hq * D:(Hq + Hkv) * D].view(N, Hkv, D).transpose(0, 1)
         if rope_desc is not None:
-            ris.rope(q, rope_desc)
-            ris.rope(k, rope_desc)
+            q = ris.rope_from(qv, torch.empty(Hq, N, D, dtype=qkv.dtype, device=qkv.device), rope_desc)
+            k = ris.rope_from(kv, torch.empty(Hkv, N, D, dtype=qkv.dtype, device=qkv.device), rope_desc)
+        else:
+            q, k = qv.contiguous(), kv.contiguous()
         desc = ris.mask_desc(mask["mode"], mask["density_ppm"], N, Hkv, n_seeds=mask["n_seeds"],
                              seed=mask.get("seed", 0), layer=l, block=mask.get("block", 0),
                              window=mask.get("window", 0), anchor=mask.get("anchor", 0))

@@ -83,6 +83,8 @@ def lib():
         L.ris_decode_attn.restype = ctypes.c_int
         L.ris_rope.argtypes = [vp, i32, i32, i64, i32, i64, ctypes.POINTER(RopeDesc), vp]
         L.ris_rope.restype = ctypes.c_int
+        L.ris_rope_from.argtypes = [vp, i64, i64, vp, i32, i32, i64, i32, i64, ctypes.POINTER(RopeDesc), vp]
+        L.ris_rope_from.restype = ctypes.c_int
         L.ris_sparse_attn.argtypes = [vp, vp, vp, vp, vp, vp, ctypes.POINTER(AttnDesc), vp]
         L.ris_sparse_attn.restype = ctypes.c_int
         L.ris_status_string.argtypes = [ctypes.c_int]
@@ -94,7 +96,7 @@ def lib():
 
 
 EXPORTS = ("ris_mask_build", "ris_mask_nnz_bound", "ris_mask_build_rows",
-           "ris_mask_rows_nnz_bound", "ris_rope", "ris_sparse_attn",
+           "ris_mask_rows_nnz_bound", "ris_rope", "ris_rope_from", "ris_sparse_attn",
            "ris_decode_workspace_bytes", "ris_decode_attn", "ris_rmsnorm", "ris_swiglu",
            "ris_status_string", "ris_version")
 
@@ -256,6 +258,20 @@ def rope(x, desc, pos0=0, stream=None):
     _check(lib().ris_rope(_ptr(x), _dtype_code(x), H, N, D, pos0, ctypes.byref(desc),
                           _stream(stream)), "ris_rope")
     return x
+
+
+def rope_from(src, out, desc, pos0=0, stream=None):
+    """ris_rope_from: src is a [heads, N, D] view (any head and token strides,
+    unit stride along D, e.g. a head-column view of a token-major projection
+    output); out is [heads, N, D] contiguous and receives the rotated rows."""
+    _need_device(out)
+    H, N, D = out.shape
+    if (not src.is_cuda or src.device != out.device or tuple(src.shape) != (H, N, D) or src.stride(2) != 1
+            or src.dtype != out.dtype):
+        raise ValueError("src must be a [heads, N, D] device view of out's dtype with unit stride along D")
+    _check(lib().ris_rope_from(_ptr(src), src.stride(0), src.stride(1), _ptr(out), _dtype_code(out), H, N, D,
+                               pos0, ctypes.byref(desc), _stream(stream)), "ris_rope_from")
+    return out
 
 
 def rope_desc(kind, base, orig_max_pos=0, factor=0.0, beta_slow=0.0, beta_fast=0.0):

@@ -33,7 +33,7 @@ def declared_functions():
 def test_header_declares_the_boundary():
     names = declared_functions()
     assert names == sorted(["ris_mask_build", "ris_mask_nnz_bound", "ris_mask_build_rows",
-                            "ris_mask_rows_nnz_bound", "ris_rope", "ris_sparse_attn",
+                            "ris_mask_rows_nnz_bound", "ris_rope", "ris_rope_from", "ris_sparse_attn",
                             "ris_decode_workspace_bytes", "ris_decode_attn", "ris_rmsnorm",
                             "ris_swiglu", "ris_status_string", "ris_version"])
 
@@ -52,7 +52,7 @@ def test_status_strings_and_version(ris):
     for code in (0, -1, -2, -3, -4, -5, -6):
         assert ris.status_string(code).startswith("RIS_")
     assert ris.status_string(123) == "unknown ris_status"
-    assert ris.version() >> 16 == 2 and ris.version() & 0xFFFF >= 2
+    assert ris.version() >> 16 == 2 and ris.version() & 0xFFFF >= 3
 
 
 def _mask(ris, **kw):
@@ -117,6 +117,12 @@ def test_rope_validation(ris):
                 ris.rope_desc(ris.ROPE_YARN, 1e6, orig_max_pos=0),
                 ris.rope_desc(ris.ROPE_LINEAR, 1e6, orig_max_pos=10, factor=-1.0)):
         assert L.ris_rope(x, 0, 1, 8, 64, 0, ctypes.byref(bad), None) == -1
+    # the strided form: null pointers and negative strides
+    assert L.ris_rope_from(None, 512, 64, x, 0, 1, 8, 64, 0, ctypes.byref(good), None) == -1
+    assert L.ris_rope_from(x, 512, 64, None, 0, 1, 8, 64, 0, ctypes.byref(good), None) == -1
+    assert L.ris_rope_from(x, -1, 64, x, 0, 1, 8, 64, 0, ctypes.byref(good), None) == -1
+    assert L.ris_rope_from(x, 512, -64, x, 0, 1, 8, 64, 0, ctypes.byref(good), None) == -1
+    assert L.ris_rope_from(x, 512, 64, x, 0, 1, 8, 63, 0, ctypes.byref(good), None) == -2
 
 
 def test_attn_validation(ris):

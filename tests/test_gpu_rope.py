@@ -67,3 +67,26 @@ def test_rope_in_place_on_long_sequence_bf16():
     want = o_rope.apply(x[:, rows], o_rope.YARN, 1e6, s=2.0, orig_max_pos=32768, positions=rows)
     tol = bf16_ulp_tol(want) + 1e-5
     assert np.all(np.abs(got[:, rows] - want) <= tol)
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_rope_from_strided_source(dtype):
+    """ris_rope_from: the head columns of a token-major [N, (Hq + 2 Hkv) D]
+    projection output, rotated into a contiguous [H, N, D] buffer, equal
+    (bit for bit) ris_rope on a contiguous copy; the source is left as it was."""
+    ris = need_gpu()
+    Hq, Hkv, N, D = 6, 2, 777, 128
+    g = torch.Generator(device="cuda")
+    g.manual_seed(5)
+    qkv = torch.randn(N, (Hq + 2 * Hkv) * D, generator=g, device="cuda").to(dtype)
+    before = qkv.clone()
+    rd = ris.rope_desc(ris.ROPE_YARN, 1e6, orig_max_pos=32768, factor=2.0)
+    for lo, H in ((0, Hq), (Hq * D, Hkv)):
+        view = qkv[:, lo:lo + H * D].view(N, H, D).transpose(0, 1)
+        out = torch.empty(H, N, D, dtype=dtype, device="cuda")
+        ris.rope_from(view, out, rd, pos0=64000)
+        ref = view.contiguous()
+        ris.rope(ref, rd, pos0=64000)
+        torch.cuda.synchronize()
+        assert torch.equal(out, ref)
+    assert torch.equal(qkv, before)
