@@ -244,8 +244,7 @@ int ris_sparse_attn(const void* Q, const void* K, const void* V, const int64_t* 
         return hip_status(ris::launch_attn_tile(a, s));
     }
     // AUTO: per 32-row tile by union density.  The tiled kernel's cost grows
-    // with the key span, the gather kernel's with the entries; on MI355X they
-    // cross near 6% (Qwen2 shape, measured).
+    // with the key span, the gather kernel's with the entries (kAutoDensity).
     a.tau = kAutoDensity;
     const int st = hip_status(ris::launch_attn_tile(a, s));
     if (st != RIS_OK) return st;
