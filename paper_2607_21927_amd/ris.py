@@ -220,6 +220,11 @@ def decode_attn(Q, K, V, pos, anchor_ptr, anchor_idx, out, workspace, desc, stre
         raise ValueError("anchor_idx must hold B * anchor_stride entries")
     if not (Q.dtype == K.dtype == V.dtype) or K.shape != V.shape:
         raise TypeError("Q, K, V must share a dtype and K, V a shape")
+    if _dtype_code(Q) != desc.dtype_in or _dtype_code(out) != desc.dtype_out:
+        raise TypeError("Q and out dtypes must match the descriptor")
+    if (tuple(Q.shape) != (desc.batch, desc.Hq, desc.D) or tuple(out.shape) != tuple(Q.shape)
+            or tuple(K.shape) != (desc.batch, desc.Hkv, desc.max_len, desc.D)):
+        raise ValueError("Q and out must be [B, Hq, D] and K, V [B, Hkv, max_len, D] as in the descriptor")
     nbytes = workspace.numel() * workspace.element_size()
     _check(lib().ris_decode_attn(_ptr(Q), _ptr(K), _ptr(V), _ptr(pos), _ptr(anchor_ptr),
                                  _ptr(anchor_idx), _ptr(out), _ptr(workspace), nbytes,
@@ -285,10 +290,22 @@ def attn_desc(Q, K, out, mode=STOCHASTIC, block=0, causal=1, scale=0.0, algo=ATT
 
 
 def sparse_attn(Q, K, V, row_ptr, col_idx, out, desc, stream=None):
-    """ris_sparse_attn: out[Hq, N, D] from the CSR sets."""
+    """ris_sparse_attn: out[Hq, N, D] from the CSR sets.  The tensors are
+    checked against the descriptor before anything is launched."""
+    import torch
     _need_device(Q, K, V, row_ptr, col_idx, out)
     if not (Q.dtype == K.dtype == V.dtype):
         raise TypeError("Q, K, V must share a dtype")
+    if _dtype_code(Q) != desc.dtype_in or _dtype_code(out) != desc.dtype_out:
+        raise TypeError("Q and out dtypes must match the descriptor")
+    q_shape, kv_shape = (desc.Hq, desc.N, desc.D), (desc.Hkv, desc.N, desc.D)
+    if tuple(Q.shape) != q_shape or tuple(out.shape) != q_shape or tuple(K.shape) != kv_shape \
+            or tuple(V.shape) != kv_shape:
+        raise ValueError(f"Q and out must be {q_shape}, K and V {kv_shape}")
+    if row_ptr.dtype != torch.int64 or row_ptr.numel() != desc.Hkv * desc.N + 1 or col_idx.dtype != torch.int32:
+        raise ValueError("row_ptr must be int64[Hkv*N + 1] and col_idx int32")
+    if len({t.device for t in (Q, K, V, row_ptr, col_idx, out)}) != 1:
+        raise ValueError("all tensors must be on one device")
     _check(lib().ris_sparse_attn(_ptr(Q), _ptr(K), _ptr(V), _ptr(row_ptr), _ptr(col_idx),
                                  _ptr(out), ctypes.byref(desc), _stream(stream)),
            "ris_sparse_attn")

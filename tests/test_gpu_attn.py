@@ -162,3 +162,26 @@ def test_auto_dispatch_mixed_density():
     assert dense.any() and (~dense).any()
     assert np.array_equal(got[:6][:, ~dense], got_g[:6][:, ~dense])
     assert np.array_equal(got[:6][:, dense], got_t[:6][:, dense])
+
+
+def test_binding_rejects_tensors_that_do_not_match_the_descriptor():
+    """The Python binding checks every tensor against the descriptor before
+    launching: a wrong shape, dtype or CSR size raises and runs nothing."""
+    from paper_2607_21927_amd import ris
+    need_gpu()
+    Hq, Hkv, N, D = 6, 2, 100, 64
+    q = torch.zeros(Hq, N, D, dtype=torch.bfloat16, device="cuda")
+    k = torch.zeros(Hkv, N, D, dtype=torch.bfloat16, device="cuda")
+    out = torch.empty(Hq, N, D, dtype=torch.float32, device="cuda")
+    rp = torch.zeros(Hkv * N + 1, dtype=torch.int64, device="cuda")
+    ci = torch.zeros(8, dtype=torch.int32, device="cuda")
+    d = ris.attn_desc(q, k, out)
+    with pytest.raises(ValueError):
+        ris.sparse_attn(q, k, k[:, :N - 1].contiguous(), rp, ci, out, d)      # V too short
+    with pytest.raises(ValueError):
+        ris.sparse_attn(q, k, k, rp[:-1].contiguous(), ci, out, d)            # row_ptr too short
+    with pytest.raises(TypeError):
+        ris.sparse_attn(q, k, k, rp, ci, out.to(torch.bfloat16), d)           # out dtype
+    with pytest.raises(ValueError):
+        big = torch.zeros(Hq, N + 1, D, dtype=torch.bfloat16, device="cuda")
+        ris.sparse_attn(big, k, k, rp, ci, out, d)                            # Q longer than N
