@@ -11,8 +11,9 @@ Modules, in the order the method runs:
 
 * ``philox``   -- Philox4x64-10 (Salmon et al., SC'11), the counter-based hash
                   keyed by (seed) and fed (query, kv-head, layer).
-* ``prp``      -- MurmurHash3 ``fmix32`` and the keyed Feistel permutation with
-                  cycle walking: an exact-k uniform draw without replacement.
+* ``prp``      -- the keyed Feistel permutation (16-bit multiply-xorshift
+                  rounds) with cycle walking: an exact-k uniform draw without
+                  replacement.
 * ``geometry`` -- density -> per-row count, Stochastic and Structural sets,
                   the seed-ensemble union and its CSR (Methods, "Memory-Bounded
                   Geometry Generation" and "Sampling Modes").

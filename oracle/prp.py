@@ -8,54 +8,69 @@ pool -- so that the density is met exactly per row and no per-seed dedupe is
 needed.  It is realised by a keyed pseudo-random permutation ``P`` of
 ``[0, n)`` and taking ``{P(0), ..., P(k-1)}``.
 
-``P`` is a Feistel network on ``m``-bit words with MurmurHash3's 32-bit
-finaliser ``fmix32`` (Appleby, public domain) as round function:
+``P`` is a Feistel network on ``m``-bit words with a keyed 16-bit
+multiply-xorshift-multiply round function:
 
 * width: ``m0 = max(2, bitlen(n-1))``; below 6 bits it is rounded up to even
   (``m`` = 2, 4 or 6), from 6 bits on ``m = m0`` -- the smallest power-of-two
   domain that holds the pool, so that cycle walking takes fewer than two
-  evaluations per draw on average;
+  evaluations per draw on average; ``m <= 32``, so a half has at most 16 bits;
 * halves: left ``a = floor(m/2)`` bits (high), right ``b = m - a`` bits (low);
-  a round replaces the left half, ``(L, R) -> (R, L xor (F(R xor k_r) mod 2^|L|))``,
-  so the half widths alternate (a, b), (b, a), ... and an even round count
-  returns to (a, b) -- the alternating split of FFX / NIST FF1 for odd widths;
-* rounds: 6 for ``m >= 6`` (halves of at least 3 bits), 12 for ``m`` = 2 or 4,
-  where 1- and 2-bit halves mix slowly;
+  a round replaces the left half, ``(L, R) -> (R, L xor F_r(R))`` with
+  ``F_r(R) < 2^|L|``, so the half widths alternate (a, b), (b, a), ... and an
+  even round count returns to (a, b) -- the alternating split of FFX / NIST
+  FF1 for odd widths;
+* round function: with key word ``k_r``, ``km = (k_r >> 16) | 1`` (odd) and
+  ``kx = k_r mod 2^16``, all arithmetic mod 2^16:
+  ``t = R km + kx;  t ^= t >> 8;  t = t C``, ``C = 0x9E37`` (the leading 16
+  bits of the golden-ratio constant 2^32/phi); ``F_r(R)`` is the top ``|L|``
+  bits of ``t``.  For every key, ``R -> t`` is a bijection of the 16-bit words
+  (an affine map with odd slope, an xorshift and an odd multiplication);
+* rounds: 6 for ``m >= 8`` (halves of at least 4 bits), 12 below, where
+  halves of 1 to 3 bits mix slowly;
 * round keys: ``k_r = w_r`` for ``r < 8`` and ``k_r = w_{r-8} xor 0x9E3779B9``
   for ``r = 8..11``, with ``w`` the eight 32-bit words of the row's Philox
   output.
+
+All operations of a round act on 16-bit words, so two draws fit one 32-bit
+register and are advanced by the same packed 16-bit instruction.
 
 Values ``>= n`` are cycle-walked (re-encrypted until they fall in range),
 which restricts a permutation of ``[0, 2^m)`` to one of ``[0, n)`` (Black and
 Rogaway, "Ciphers with arbitrary finite domains", 2002).
 
-Pinned by: ``fmix32`` against scikit-learn's MurmurHash3 of the empty string
-(which reduces to ``fmix32(seed)``); exhaustive bijectivity for every width up
-to 16 bits; distinctness and range of cycle-walked draws; chi-square
-uniformity over independent keys of inclusion, of the first draw and of the
-ordered pair (P(0), P(1)).  The particular permutation is a definitional
-choice (any uniform draw realises the paper's sampling); the GPU reproduces it
-bit for bit.
+Pinned by: the 16-bit map ``R -> t`` is a bijection for every key (an even
+slope would break it); exhaustive bijectivity of the network for every width
+up to 16 bits; distinctness and range of cycle-walked draws; chi-square
+uniformity over independent keys of inclusion, of the first draw, of the
+ordered pair (P(0), P(1)) and of the ordered triple (P(0), P(1), P(2)).  The
+particular permutation is a definitional choice (any uniform draw realises the
+paper's sampling); the GPU reproduces it bit for bit.
 """
 
 import numpy as np
 
-_M32 = np.uint64(0xFFFFFFFF)
-FMIX_C1 = np.uint64(0x85EBCA6B)
-FMIX_C2 = np.uint64(0xC2B2AE35)
+_M16 = np.uint64(0xFFFF)
+MIX_C = np.uint64(0x9E37)
 KEY_TWEAK = np.uint64(0x9E3779B9)
 WORDS = 8          # row words (round-key material)
 
 
-def fmix32(h):
-    """MurmurHash3 32-bit finaliser on uint64 arrays holding 32-bit values."""
-    h = np.asarray(h, dtype=np.uint64) & _M32
-    h = h ^ (h >> np.uint64(16))
-    h = (h * FMIX_C1) & _M32
-    h = h ^ (h >> np.uint64(13))
-    h = (h * FMIX_C2) & _M32
-    h = h ^ (h >> np.uint64(16))
-    return h
+def mix16(r, k):
+    """The keyed 16-bit mixing map t(R) of one round (before the top bits are
+    taken): uint64 arrays, r < 2^16, k a 32-bit key word."""
+    r = np.asarray(r, dtype=np.uint64)
+    k = np.asarray(k, dtype=np.uint64)
+    km = ((k >> np.uint64(16)) & _M16) | np.uint64(1)
+    kx = k & _M16
+    t = (r * km + kx) & _M16
+    t = t ^ (t >> np.uint64(8))
+    return (t * MIX_C) & _M16
+
+
+def round_fn(r, k, width):
+    """F_r(R): the top ``width`` bits (1..16) of mix16(R, k_r)."""
+    return mix16(r, k) >> np.uint64(16 - width)
 
 
 def domain_bits(n):
@@ -73,7 +88,7 @@ def domain_bits(n):
 
 def rounds(m):
     """Round count for width m (a scalar)."""
-    return 6 if m >= 6 else 12
+    return 6 if m >= 8 else 12
 
 
 def round_key(w, r):
@@ -87,6 +102,7 @@ def feistel(x, w, m):
     x: uint64 array of values < 2^m.  w: uint64 array (..., 8) of row words
     with leading shape equal to x's.  m: a scalar width from domain_bits.
     """
+    assert 2 <= m <= 32, m
     x = np.asarray(x, dtype=np.uint64)
     a = m // 2
     b = m - a
@@ -94,7 +110,7 @@ def feistel(x, w, m):
     right = x & np.uint64((1 << b) - 1)
     wl, wr = a, b
     for r in range(rounds(m)):
-        f = fmix32(right ^ round_key(w, r)) & np.uint64((1 << wl) - 1)
+        f = round_fn(right, round_key(w, r), wl)
         left, right = right, left ^ f
         wl, wr = wr, wl
     return (left << np.uint64(wr)) | right

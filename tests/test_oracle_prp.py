@@ -2,55 +2,71 @@
 import numpy as np
 import pytest
 from scipy.stats import chi2
-from sklearn.utils import murmurhash3_32
 
 from oracle import prp
 
 
-def test_fmix32_against_sklearn_murmurhash3():
-    """MurmurHash3_x86_32 of the empty string with seed x is fmix32(x)."""
+def test_round_mixer_is_a_bijection_of_16_bit_words():
+    """For every key the 16-bit map of a round (affine with odd slope,
+    xorshift, odd multiplication) permutes [0, 2^16); a slope that lost its
+    forced low bit would collapse half the words."""
     rng = np.random.default_rng(1)
-    xs = np.concatenate([[0, 1, 2, 0xFFFFFFFF, 0x80000000],
-                         rng.integers(0, 2**32, size=3000, dtype=np.uint64)])
-    got = prp.fmix32(xs.astype(np.uint64))
-    want = np.array([murmurhash3_32(b"", seed=int(x), positive=True) for x in xs], dtype=np.uint64)
-    assert np.array_equal(got, want)
-    assert int(prp.fmix32(np.uint64(1))) == 0x514E28B7   # published test vector
+    r = np.arange(1 << 16, dtype=np.uint64)
+    keys = np.concatenate([[0, 1, 0xFFFF, 0x10000, 0xFFFFFFFF, 0x9E3779B9],
+                           rng.integers(0, 2**32, size=40, dtype=np.uint64)])
+    for k in keys:
+        t = prp.mix16(r, np.uint64(k))
+        assert t.max() < (1 << 16)
+        assert np.unique(t).size == (1 << 16), hex(int(k))
+    # the same map with an even slope (the low bit of the high key half
+    # cleared) is not one: the pin above can fail
+    even = ((r * np.uint64(0x9E36)) & np.uint64(0xFFFF))
+    assert np.unique(even).size < (1 << 16)
+
+
+def test_round_function_takes_the_top_bits():
+    rng = np.random.default_rng(2)
+    r = rng.integers(0, 1 << 16, size=500, dtype=np.uint64)
+    k = rng.integers(0, 2**32, size=500, dtype=np.uint64)
+    t = prp.mix16(r, k)
+    for w in range(1, 17):
+        f = prp.round_fn(r, k, w)
+        assert f.max() < (1 << w)
+        assert np.array_equal(f, t >> np.uint64(16 - w))
 
 
 def test_domain_bits_and_rounds():
     ns = [1, 2, 3, 4, 5, 8, 9, 16, 17, 32, 33, 64, 65, 4096, 4097, 65536, 65537, 262144]
     want = [2, 2, 2, 2, 4, 4, 4, 4, 6, 6, 6, 6, 7, 12, 13, 16, 17, 18]
     assert list(prp.domain_bits(np.array(ns))) == want
-    assert [prp.rounds(m) for m in (2, 4, 6, 7, 18)] == [12, 12, 6, 6, 6]
+    assert [prp.rounds(m) for m in (2, 4, 6, 7, 8, 18, 32)] == [12, 12, 12, 12, 6, 6, 6]
     # the domain never exceeds twice the pool once the width is exact (n > 32)
     for n in [33, 100, 1000, 65536, 65537, 262144]:
         assert (1 << int(prp.domain_bits(n))) < 2 * n
 
 
 def test_feistel_matches_a_plain_python_rewrite():
-    """The vectorised rounds equal a scalar rewrite of the stated network."""
+    """The vectorised rounds equal a scalar rewrite of the stated network
+    (a consistency check of the vectorisation, not a pin)."""
     rng = np.random.default_rng(7)
-    M = 0xFFFFFFFF
 
-    def fmix(h):
-        h ^= h >> 16
-        h = (h * 0x85EBCA6B) & M
-        h ^= h >> 13
-        h = (h * 0xC2B2AE35) & M
-        return h ^ (h >> 16)
+    def F(right, k, width):
+        km, kx = (k >> 16) | 1, k & 0xFFFF
+        t = (right * km + kx) & 0xFFFF
+        t ^= t >> 8
+        t = (t * 0x9E37) & 0xFFFF
+        return t >> (16 - width)
 
-    for m in [2, 4, 6, 7, 9, 16, 17]:
+    for m in [2, 4, 6, 7, 8, 9, 16, 17, 31, 32]:
         w = [int(v) for v in rng.integers(0, 2**32, size=8, dtype=np.uint64)]
         xs = rng.integers(0, 1 << m, size=40, dtype=np.uint64)
         got = prp.feistel(xs, np.broadcast_to(np.array(w, dtype=np.uint64), (40, 8)), m)
         a, b = m // 2, m - m // 2
         for x, g in zip(xs, got):
             left, right, wl = int(x) >> b, int(x) & ((1 << b) - 1), a
-            for r in range(12 if m < 6 else 6):
+            for r in range(12 if m < 8 else 6):
                 k = w[r] if r < 8 else w[r - 8] ^ 0x9E3779B9
-                f = fmix(right ^ k) & ((1 << wl) - 1)
-                left, right = right, left ^ f
+                left, right = right, left ^ F(right, k, wl)
                 wl = b if wl == a and r % 2 == 0 else a
             assert ((left << b) | right) == int(g)
 
@@ -107,7 +123,7 @@ def test_inclusion_and_first_draw_are_uniform(n, k):
     assert ok, stat
 
 
-@pytest.mark.parametrize("n", [4, 5, 7, 9, 16, 17, 32, 33, 65])
+@pytest.mark.parametrize("n", [4, 5, 7, 9, 16, 17, 32, 33, 65, 129, 257])
 def test_successive_draws_are_jointly_uniform(n):
     """(P(0), P(1)) is uniform over ordered pairs of distinct keys, one pair
     per independent key (so the cells are a true multinomial); widths with
@@ -118,6 +134,47 @@ def test_successive_draws_are_jointly_uniform(n):
     off = ~np.eye(n, dtype=bool)
     assert counts[~off].sum() == 0
     ok, stat = _chi2_ok(counts[off], trials / (n * (n - 1)), n * (n - 1) - 1)
+    assert ok, stat
+
+
+@pytest.mark.parametrize("n", [5, 9, 17, 33])
+def test_three_successive_draws_are_jointly_uniform(n):
+    """(P(0), P(1), P(2)) is uniform over ordered triples of distinct keys,
+    one triple per independent key (12-round widths)."""
+    trials = 25 * n * (n - 1) * (n - 2)
+    x = _draws(n, 3, trials, 2000 + n)
+    cell = (x[:, 0] * n + x[:, 1]) * n + x[:, 2]
+    counts = np.bincount(cell, minlength=n ** 3)
+    i = np.arange(n ** 3)
+    a, b, c = i // (n * n), (i // n) % n, i % n
+    distinct = (a != b) & (b != c) & (a != c)
+    assert counts[~distinct].sum() == 0
+    ok, stat = _chi2_ok(counts[distinct], trials / distinct.sum(), int(distinct.sum()) - 1)
+    assert ok, stat
+
+
+@pytest.mark.parametrize("n", [300, 4097, 65537])
+def test_draws_on_large_pools_are_jointly_uniform_in_bins(n):
+    """On six-round widths: (P(j), P(j+1)) for j = 0 and 7 in 32 x 32 bins,
+    and (P(0), P(1), P(2)) in 16^3 bins, over independent keys."""
+    rng = np.random.default_rng(3000 + n)
+    trials = 100000
+    for j0 in (0, 7):
+        keys = rng.integers(0, 2**32, size=(trials, 8), dtype=np.uint64)
+        j = np.tile(np.array([j0, j0 + 1], dtype=np.uint64), trials)
+        x = prp.permute(j, np.repeat(keys, 2, axis=0), n).astype(np.int64).reshape(trials, 2)
+        bins = x * 32 // n
+        # bin masses: equal up to the pool not dividing into 32 bins
+        mass = np.bincount(np.arange(n) * 32 // n, minlength=32) / n
+        expect = trials * np.outer(mass, mass).ravel()
+        ok, stat = _chi2_ok(np.bincount(bins[:, 0] * 32 + bins[:, 1], minlength=1024), expect, 1023)
+        assert ok, (j0, stat)
+    x = _draws(n, 3, 200000, 4000 + n)
+    bins = x * 16 // n
+    mass = np.bincount(np.arange(n) * 16 // n, minlength=16) / n
+    expect = 200000 * np.einsum("i,j,k->ijk", mass, mass, mass).ravel()
+    cell = (bins[:, 0] * 16 + bins[:, 1]) * 16 + bins[:, 2]
+    ok, stat = _chi2_ok(np.bincount(cell, minlength=4096), expect, 4095)
     assert ok, stat
 
 
