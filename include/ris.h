@@ -70,8 +70,10 @@ typedef enum { RIS_ATTN_AUTO = 0, RIS_ATTN_GATHER = 1, RIS_ATTN_TILE = 2 } ris_a
  * k_g = min(bB, max(0, k(q) - (q - bB + 1))) keys drawn uniformly from
  * [0, bB): the clique's cost is deducted from the global budget (Methods,
  * "Sampling Modes", Structural).  The draw of seed s for row (layer, kv_head,
- * q) is a keyed Feistel permutation of the pool whose six round keys are the
- * first six 32-bit words of Philox4x64-10(counter = (q, kv_head, layer, 0),
+ * q) is {P(0), ..., P(k-1)} for P a keyed Feistel permutation of the pool
+ * (m-bit words, m = bitlen(n-1) with small-pool adjustments, cycle walking;
+ * 16-bit multiply-xorshift rounds, 6 from 8 bits on and 12 below) whose round
+ * keys are the 32-bit words of Philox4x64-10(counter = (q, kv_head, layer, 0),
  * key = (s, 0)); a keyed permutation yields distinct keys with no dedupe.
  *
  * The full geometry adds two contiguous ranges to the same union (Methods,
@@ -314,7 +316,8 @@ const char* ris_status_string(int status);
 /* Library ABI version: (major << 16) | minor.  2.0 added window and anchor to
  * ris_mask_desc; 2.1 added the row-range build and the decode step; 2.2 the
  * host-model layers (RMSNorm, SwiGLU); 2.3 the strided rotation
- * ris_rope_from. */
+ * ris_rope_from; 2.4 changed the draws' round function (the same descriptor
+ * now yields different, equally distributed sets). */
 int ris_version(void);
 
 #ifdef __cplusplus

@@ -65,45 +65,91 @@ typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 // One lane's share of the batch's (seed, draw) pairs, OR-ed into the bitmap.
 // Lane t takes the contiguous flat indices [t per, (t+1) per) (flat index =
-// seed * draws + draw), so its seed -- and the round keys it holds -- changes
-// at most a few times per batch.  Each lane walks its draws one permutation
-// step per iteration: a lane whose value lands in the pool emits it and starts
-// its next draw at once, so cycle walks of different lengths do not hold the
-// wave at the slowest lane.  Every walk returns to the pool within the domain
-// size (the cycle through j < n returns to j), so per * size iterations bound
-// the loop; the bound is a wave-uniform counter.
+// seed * draws + draw) and splits them between two walkers, A (first half) and
+// B (second half), held in the low and high 16-bit halves of the same
+// registers, so that one packed round advances both.  A walker's seed -- and
+// the round keys it holds -- changes at most a few times per batch.  Each
+// walker moves one permutation step per iteration: a walker whose value lands
+// in the pool emits it and starts its next draw at once, so cycle walks of
+// different lengths do not hold the wave at the slowest lane.  Every walk
+// returns to the pool within the domain size (the cycle through j < n returns
+// to j), so half * size iterations bound the loop; the bound is a wave-uniform
+// counter.
 template <int ROUNDS>
 __device__ __forceinline__ void walk_draws(const FeistelDomain& dom, const uint32_t* rks,
                                            uint32_t* bits, uint32_t total, uint32_t draws,
                                            float inv_draws) {
     const uint32_t per = (total + kThreads - 1) / kThreads;
-    uint32_t idx = threadIdx.x * per;
-    const uint32_t end = min(idx + per, total);
-    if (idx >= end) return;
-    int s = 0, j = 0;
-    split_draw(idx, draws, inv_draws, s, j);
-    uint32_t w[kRowWords];
-    auto load_words = [&]() {
-        const u32x4_t w0 = *reinterpret_cast<const u32x4_t*>(&rks[s * kRowWords]);
-        const u32x4_t w1 = *reinterpret_cast<const u32x4_t*>(&rks[s * kRowWords + 4]);
-        w[0] = w0.x; w[1] = w0.y; w[2] = w0.z; w[3] = w0.w;
-        w[4] = w1.x; w[5] = w1.y; w[6] = w1.z; w[7] = w1.w;
+    const uint32_t lo = threadIdx.x * per;
+    const uint32_t hi = min(lo + per, total);
+    if (lo >= hi) return;
+    const uint32_t half = (hi - lo + 1) / 2;
+    uint32_t idxA = lo, idxB = lo + half;
+    const uint32_t endA = lo + half, endB = hi;
+    bool doneA = false, doneB = idxB >= endB;
+    int sA = 0, jA = 0, sB = 0, jB = 0;
+    split_draw(idxA, draws, inv_draws, sA, jA);
+    if (!doneB) split_draw(idxB, draws, inv_draws, sB, jB);
+    // Round keys, packed: multiplier (k >> 16) | 1 and offset k & 0xFFFF of
+    // walker A in the low half, of walker B in the high half.
+    uint32_t KM[ROUNDS], KX[ROUNDS];
+    auto key = [&](int s, int r) -> uint32_t {
+        return r < kRowWords ? rks[s * kRowWords + r] : (rks[s * kRowWords + r - kRowWords] ^ kKeyTweak);
     };
-    load_words();
-    uint32_t x = (uint32_t)j;
-    const uint64_t max_it = (uint64_t)per * dom.size;
-    for (uint64_t it = 0; it < max_it; ++it) {
-        x = feistel<ROUNDS>(x, w, dom.a, dom.b);
-        if (x < dom.n) {
-            atomicOr(&bits[x >> 5], 1u << (x & 31u));
-            if (++idx == end) break;
-            if (++j == (int)draws) {
-                j = 0;
-                ++s;
-                load_words();
-            }
-            x = (uint32_t)j;
+    auto load_A = [&]() {
+#pragma unroll
+        for (int r = 0; r < ROUNDS; ++r) {
+            const uint32_t k = key(sA, r);
+            KM[r] = (KM[r] & 0xFFFF0000u) | (k >> 16) | 1u;
+            KX[r] = (KX[r] & 0xFFFF0000u) | (k & 0xFFFFu);
         }
+    };
+    auto load_B = [&]() {
+#pragma unroll
+        for (int r = 0; r < ROUNDS; ++r) {
+            const uint32_t k = key(sB, r);
+            KM[r] = (KM[r] & 0xFFFFu) | (k & 0xFFFF0000u) | 0x10000u;
+            KX[r] = (KX[r] & 0xFFFFu) | (k << 16);
+        }
+    };
+#pragma unroll
+    for (int r = 0; r < ROUNDS; ++r) { KM[r] = 0x00010001u; KX[r] = 0u; }
+    load_A();
+    if (!doneB) load_B();
+    const uint32_t b = dom.b, mb = (1u << b) - 1u, n = dom.n;
+    const u16x2_t sh_a = {(unsigned short)(16u - dom.a), (unsigned short)(16u - dom.a)};
+    const u16x2_t sh_b = {(unsigned short)(16u - b), (unsigned short)(16u - b)};
+    uint32_t xA = (uint32_t)jA, xB = (uint32_t)jB;
+    const uint64_t max_it = (uint64_t)half * dom.size;
+    for (uint64_t it = 0; it < max_it; ++it) {
+        uint32_t L = (xA >> b) | ((xB >> b) << 16);
+        uint32_t R = (xA & mb) | ((xB & mb) << 16);
+#pragma unroll
+        for (int r = 0; r < ROUNDS; ++r) feistel_round_x2(L, R, KM[r], KX[r], (r & 1) ? sh_b : sh_a);
+        // An even round count leaves widths (a, b): the value is L << b | R.
+        xA = ((L & 0xFFFFu) << b) | (R & 0xFFFFu);
+        xB = ((L >> 16) << b) | (R >> 16);
+        if (!doneA && xA < n) {
+            atomicOr(&bits[xA >> 5], 1u << (xA & 31u));
+            doneA = ++idxA == endA;
+            if (++jA == (int)draws) {
+                jA = 0;
+                ++sA;
+                if (!doneA) load_A();
+            }
+            xA = (uint32_t)jA;
+        }
+        if (!doneB && xB < n) {
+            atomicOr(&bits[xB >> 5], 1u << (xB & 31u));
+            doneB = ++idxB == endB;
+            if (++jB == (int)draws) {
+                jB = 0;
+                ++sB;
+                if (!doneB) load_B();
+            }
+            xB = (uint32_t)jB;
+        }
+        if (doneA && doneB) break;
     }
 }
 

@@ -100,7 +100,7 @@ constexpr float kAutoDensity = 0.068f;
 
 extern "C" {
 
-int ris_version(void) { return (2 << 16) | 3; }
+int ris_version(void) { return (2 << 16) | 4; }
 
 const char* ris_status_string(int status) {
     switch (status) {

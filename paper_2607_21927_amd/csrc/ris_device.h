@@ -43,20 +43,16 @@ __device__ __forceinline__ void row_round_keys(uint64_t seed, uint64_t q, uint64
     }
 }
 
-// MurmurHash3 32-bit finaliser.
-__device__ __forceinline__ uint32_t fmix32(uint32_t h) {
-    h ^= h >> 16; h *= 0x85EBCA6Bu;
-    h ^= h >> 13; h *= 0xC2B2AE35u;
-    h ^= h >> 16;
-    return h;
-}
-
 // Keyed permutation of [0, n) used for exact-k draws: a Feistel network on
-// m-bit words with fmix32 rounds, restricted to [0, n) by cycle walking.
-// m = max(2, bitlen(n - 1)), rounded up to even below 6 bits; left half
-// a = m/2 bits (high), right half b = m - a (low); each round replaces the
-// left half, so the widths alternate (a, b), (b, a), ...; 6 rounds from 6 bits
-// on, 12 below.  Round key r is word r, or word r - 8 xor 0x9E3779B9.
+// m-bit words, restricted to [0, n) by cycle walking.  m = max(2,
+// bitlen(n - 1)), rounded up to even below 6 bits; left half a = m/2 bits
+// (high), right half b = m - a (low); each round replaces the left half, so
+// the widths alternate (a, b), (b, a), ...; 6 rounds from 8 bits on, 12
+// below.  Round r, key word k (word r, or word r - 8 xor 0x9E3779B9), all on
+// 16-bit words: t = R * ((k >> 16) | 1) + (k & 0xFFFF); t ^= t >> 8;
+// t *= 0x9E37; the round value is the top |L| bits of t.  Halves never exceed
+// 16 bits (m <= 32), so two draws share a register, one per 16-bit half, and
+// one packed 16-bit instruction advances both.
 struct FeistelDomain {
     uint32_t n;       // pool size (>= 1)
     uint32_t a, b;    // left / right half widths
@@ -71,26 +67,30 @@ __host__ __device__ __forceinline__ FeistelDomain make_domain(uint32_t n) {
     if (bits < 6) bits += bits & 1u;
     FeistelDomain d;
     d.n = n; d.a = bits / 2; d.b = bits - d.a;
-    d.rounds = bits >= 6 ? 6u : 12u;
+    d.rounds = bits >= 8 ? 6u : 12u;
     d.size = 1u << bits;
     return d;
 }
 
 constexpr uint32_t kKeyTweak = 0x9E3779B9u;
+constexpr unsigned short kMixMul = 0x9E37;
 
-template <int ROUNDS>
-__device__ __forceinline__ uint32_t feistel(uint32_t x, const uint32_t w[kRowWords], uint32_t a,
-                                            uint32_t b) {
-    uint32_t L = x >> b, R = x & ((1u << b) - 1u);
-#pragma unroll
-    for (int r = 0; r < ROUNDS; ++r) {
-        const uint32_t wl = (r & 1) ? b : a;          // width of the half being replaced
-        const uint32_t k = r < kRowWords ? w[r] : (w[r - kRowWords] ^ kKeyTweak);
-        const uint32_t f = fmix32(R ^ k) & ((1u << wl) - 1u);
-        const uint32_t t = L ^ f;
-        L = R; R = t;
-    }
-    return (L << b) | R;
+typedef unsigned short u16x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ u16x2_t as_u16x2(uint32_t v) { return __builtin_bit_cast(u16x2_t, v); }
+__device__ __forceinline__ uint32_t as_u32(u16x2_t v) { return __builtin_bit_cast(uint32_t, v); }
+
+// One round on two draws at once.  L and R hold the two draws' half words in
+// their low and high 16 bits; km and kx pack the two draws' round multipliers
+// ((k >> 16) | 1) and offsets (k & 0xFFFF); shift = 16 - width of L.
+__device__ __forceinline__ void feistel_round_x2(uint32_t& L, uint32_t& R, uint32_t km, uint32_t kx,
+                                                 u16x2_t shift) {
+    u16x2_t t = as_u16x2(R) * as_u16x2(km) + as_u16x2(kx);
+    t ^= t >> (u16x2_t){8, 8};
+    t *= (u16x2_t){kMixMul, kMixMul};
+    t = t >> shift;
+    const uint32_t nr = L ^ as_u32(t);
+    L = R;
+    R = nr;
 }
 
 // Count rule: clamp(round_half_up(ppm * n / 1e6), 1, n).

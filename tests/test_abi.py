@@ -52,7 +52,7 @@ def test_status_strings_and_version(ris):
     for code in (0, -1, -2, -3, -4, -5, -6):
         assert ris.status_string(code).startswith("RIS_")
     assert ris.status_string(123) == "unknown ris_status"
-    assert ris.version() >> 16 == 2 and ris.version() & 0xFFFF >= 3
+    assert ris.version() >> 16 == 2 and ris.version() & 0xFFFF >= 4
 
 
 def _mask(ris, **kw):
