@@ -31,6 +31,11 @@ ROW_CASES = [
     (1, 50_000, 3000, 4, 10, 64, 0, 0, 2999, 1),
     (1, 10_000, 3000, 2, 10, 64, 128, 4, 700, 129),
     (0, 30_000, 2000, 1, 4, 0, 64, 3, 0, 1),
+    # the longest sequences: pools across 2^17 (17- to 18-bit domains) and
+    # the last rows of RIS_MAX_N
+    (0, 10_000, 262144, 1, 3, 0, 0, 0, 131000, 100),
+    (0, 2_000, 262144, 2, 5, 0, 0, 0, 262080, 64),
+    (1, 10_000, 262144, 1, 3, 64, 1024, 4, 262100, 44),
 ]
 
 
