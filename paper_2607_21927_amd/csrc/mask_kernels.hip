@@ -218,7 +218,7 @@ __device__ __forceinline__ uint32_t block_sum(uint32_t v, uint32_t* red) {
 // Exclusive prefix of v over the block; *total receives the block sum.
 __device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* red, uint32_t* total) {
     const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-    const uint32_t inc = wave_inclusive_scan(v, lane);
+    const uint32_t inc = wave_inclusive_scan(v);
     if (lane == 63) red[wid] = inc;
     __syncthreads();
     uint32_t before = 0;
