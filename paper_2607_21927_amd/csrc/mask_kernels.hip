@@ -392,8 +392,14 @@ __global__ __launch_bounds__(kThreads) void k_mask_fused(MaskParams p, int64_t* 
                 __builtin_amdgcn_s_sleep(1);
                 continue;
             }
-            int64_t part = lane <= first ? (v & kValueMask) : 0;
-            for (int off = 32; off > 0; off >>= 1) part += __shfl_xor(part, off);
+            // Lanes before `first` hold single row counts (below 2^32); lane
+            // `first` holds an inclusive prefix.
+            int64_t part = (int64_t)wave_sum_u32(lane < first ? (uint32_t)(v & kValueMask) : 0u);
+            if (first < 64) {
+                const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, first);
+                const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)((uint64_t)v >> 32), first);
+                part += (int64_t)((((uint64_t)hi << 32) | lo) & (uint64_t)kValueMask);
+            }
             prefix += part;
             if (first < 64) break;
             j -= 64;
