@@ -65,16 +65,18 @@ typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 // One lane's share of the batch's (seed, draw) pairs, OR-ed into the bitmap.
 // Lane t takes the contiguous flat indices [t per, (t+1) per) (flat index =
-// seed * draws + draw) and splits them between two walkers, A (first half) and
-// B (second half), held in the low and high 16-bit halves of the same
-// registers, so that one packed round advances both.  A walker's seed -- and
+// seed * draws + draw) and works through them with two walkers held in the
+// low and high 16-bit halves of the same registers, so that one packed round
+// advances both: walker A takes the lane's draws from the front, walker B
+// from the back, until they meet; the lane ends when its last draw is done
+// rather than when the slower of two fixed halves is.  A walker's seed -- and
 // the round keys it holds -- changes at most a few times per batch.  Each
 // walker moves one permutation step per iteration: a walker whose value lands
 // in the pool emits it and starts its next draw at once, so cycle walks of
 // different lengths do not hold the wave at the slowest lane.  Every walk
 // returns to the pool within the domain size (the cycle through j < n returns
-// to j), so half * size iterations bound the loop; the bound is a wave-uniform
-// counter.
+// to j), and every iteration advances an unfinished draw, so per * size
+// iterations bound the loop; the bound is a wave-uniform counter.
 template <int ROUNDS>
 __device__ __forceinline__ void walk_draws(const FeistelDomain& dom, const uint32_t* rks,
                                            uint32_t* bits, uint32_t total, uint32_t draws,
@@ -83,15 +85,13 @@ __device__ __forceinline__ void walk_draws(const FeistelDomain& dom, const uint3
     const uint32_t lo = threadIdx.x * per;
     const uint32_t hi = min(lo + per, total);
     if (lo >= hi) return;
-    const uint32_t half = (hi - lo + 1) / 2;
-    uint32_t idxA = lo, idxB = lo + half;
-    const uint32_t endA = lo + half, endB = hi;
-    bool doneA = false, doneB = idxB >= endB;
+    // Walker A takes the lane's draws from the front, walker B from the back;
+    // `rest` counts the draws neither has started.
+    bool actA = true, actB = hi - lo >= 2;
+    uint32_t rest = hi - lo - (actB ? 2u : 1u);
     int sA = 0, jA = 0, sB = 0, jB = 0;
-    split_draw(idxA, draws, inv_draws, sA, jA);
-    if (!doneB) split_draw(idxB, draws, inv_draws, sB, jB);
-    // Round keys, packed: multiplier (k >> 16) | 1 and offset k & 0xFFFF of
-    // walker A in the low half, of walker B in the high half.
+    split_draw(lo, draws, inv_draws, sA, jA);
+    if (actB) split_draw(hi - 1, draws, inv_draws, sB, jB);
     uint32_t KM[ROUNDS], KX[ROUNDS];
     auto key = [&](int s, int r) -> uint32_t {
         return r < kRowWords ? rks[s * kRowWords + r] : (rks[s * kRowWords + r - kRowWords] ^ kKeyTweak);
@@ -115,41 +115,49 @@ __device__ __forceinline__ void walk_draws(const FeistelDomain& dom, const uint3
 #pragma unroll
     for (int r = 0; r < ROUNDS; ++r) { KM[r] = 0x00010001u; KX[r] = 0u; }
     load_A();
-    if (!doneB) load_B();
+    if (actB) load_B();
     const uint32_t b = dom.b, mb = (1u << b) - 1u, n = dom.n;
     const u16x2_t sh_a = {(unsigned short)(16u - dom.a), (unsigned short)(16u - dom.a)};
     const u16x2_t sh_b = {(unsigned short)(16u - b), (unsigned short)(16u - b)};
     uint32_t xA = (uint32_t)jA, xB = (uint32_t)jB;
-    const uint64_t max_it = (uint64_t)half * dom.size;
+    const uint64_t max_it = (uint64_t)(hi - lo) * dom.size;
     for (uint64_t it = 0; it < max_it; ++it) {
         uint32_t L = (xA >> b) | ((xB >> b) << 16);
         uint32_t R = (xA & mb) | ((xB & mb) << 16);
 #pragma unroll
         for (int r = 0; r < ROUNDS; ++r) feistel_round_x2(L, R, KM[r], KX[r], (r & 1) ? sh_b : sh_a);
-        // An even round count leaves widths (a, b): the value is L << b | R.
         xA = ((L & 0xFFFFu) << b) | (R & 0xFFFFu);
         xB = ((L >> 16) << b) | (R >> 16);
-        if (!doneA && xA < n) {
+        if (actA && xA < n) {
             atomicOr(&bits[xA >> 5], 1u << (xA & 31u));
-            doneA = ++idxA == endA;
-            if (++jA == (int)draws) {
-                jA = 0;
-                ++sA;
-                if (!doneA) load_A();
+            if (rest == 0u) {
+                actA = false;
+            } else {
+                --rest;
+                if (++jA == (int)draws) {
+                    jA = 0;
+                    ++sA;
+                    load_A();
+                }
+                xA = (uint32_t)jA;
             }
-            xA = (uint32_t)jA;
         }
-        if (!doneB && xB < n) {
+        if (actB && xB < n) {
             atomicOr(&bits[xB >> 5], 1u << (xB & 31u));
-            doneB = ++idxB == endB;
-            if (++jB == (int)draws) {
-                jB = 0;
-                ++sB;
-                if (!doneB) load_B();
+            if (rest == 0u) {
+                actB = false;
+            } else {
+                --rest;
+                if (jB == 0) {
+                    jB = (int)draws;
+                    --sB;
+                    load_B();
+                }
+                --jB;
+                xB = (uint32_t)jB;
             }
-            xB = (uint32_t)jB;
         }
-        if (doneA && doneB) break;
+        if (!actA && !actB) break;
     }
 }
 
