@@ -71,3 +71,35 @@ def test_workload_end_to_end(name):
         worst = max(worst, float(np.abs(got[h, q] - want).max()))
     say(f"  {len(rows)} sampled rows, max err {worst:.3e}")
     assert worst <= 2e-2
+
+
+def test_needle_recall_structural_32k():
+    """Quality probe of the Structural workload's planted pairs (p, i): a
+    needle inside query i's block clique is always in I(i); outside it, p is
+    drawn by at least one of the S seeds with probability
+    1 - (1 - k_g(i) / bB(i))^S (each seed's draw is uniform over the pool
+    [0, bB); Methods, "Sampling Modes", Structural, and the capture
+    probability of "Ensemble Stochastic Projection and Retrieval Coverage").
+    The GPU geometry's recall over every planted pair and both KV heads must
+    match the mean of those probabilities within 5 standard errors."""
+    ris = need_gpu()
+    w = WORKLOADS["qwen2_32k_structural"]
+    sp = spec_of(w.mode, w.density_ppm, w.N, w.Hkv, w.n_seeds, w.seed, 0, 1, w.block)
+    say("needle recall qwen2_32k_structural")
+    rp_d, ci_d = ris.build_csr(desc_of(ris, sp), "cuda", use_bound=True)
+    rp = rp_d.cpu().numpy()
+    ci = ci_d[: int(rp[-1])].cpu().numpy()
+    p, i = needle_plan(w.N)
+    n, kg, start = o_geo._pool_and_draws(sp, i)
+    inside = p >= start
+    prob = np.where(n > 0, 1.0 - (1.0 - kg / np.maximum(n, 1)) ** w.n_seeds, 0.0)
+    for g in range(w.Hkv):
+        rows = g * w.N + i
+        lo, hi = rp[rows], rp[rows + 1]
+        hit = np.array([ci[a + np.searchsorted(ci[a:b], pp)] == pp if np.searchsorted(ci[a:b], pp) < b - a
+                        else False for a, b, pp in zip(lo, hi, p)])
+        assert hit[inside].all()
+        out = ~inside
+        got, want = hit[out].mean(), prob[out].mean()
+        se = np.sqrt((prob[out] * (1 - prob[out])).sum()) / out.sum()
+        assert abs(got - want) < 5 * se, (g, got, want, se)
