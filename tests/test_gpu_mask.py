@@ -139,3 +139,26 @@ def test_mask_full_size(name):
         want = o_geo.row_sets(sp, h, np.array([qq]))[0]
         assert np.array_equal(g, want), (h, qq)
     say(f"  nnz = {rp[-1]} ({rp[-1] / (w.Hkv * w.N * (w.N + 1) / 2):.4f} of causal pairs)")
+
+
+@pytest.mark.parametrize("name", ["qwen2_32k_stochastic", "qwen2_64k_stochastic_yarn"])
+def test_union_size_matches_its_expectation(name):
+    """Statistical pin of the permutation at full size: with each seed's set
+    a uniform k-subset of the pool, a key is in the union with probability
+    P = 1 - (1 - k/n)^S (Eq. union coverage), so E[nnz] = sum n P over the
+    rows; the inclusion indicators of one row are negatively correlated
+    (exact-k draws), so sum n P (1 - P) bounds the variance.  The GPU nnz
+    must lie within 5 standard deviations."""
+    from synth import WORKLOADS
+    ris = need_gpu()
+    w = WORKLOADS[name]
+    sp = spec_of(w.mode, w.density_ppm, w.N, w.Hkv, w.n_seeds, w.seed, 0, 1)
+    say(f"union size {name}")
+    rp, _ = gpu_csr(ris, sp, use_bound=True)
+    nnz = int(rp[-1].item())
+    n = np.arange(1, w.N + 1, dtype=np.float64)
+    k = o_geo.row_count(w.density_ppm, n.astype(np.int64)).astype(np.float64)
+    P = 1.0 - (1.0 - k / n) ** w.n_seeds
+    mean = w.Hkv * float((n * P).sum())
+    sd = np.sqrt(w.Hkv * float((n * P * (1.0 - P)).sum()))
+    assert abs(nnz - mean) < 5 * sd, (nnz, mean, sd)
