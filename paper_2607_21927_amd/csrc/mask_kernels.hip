@@ -75,8 +75,8 @@ typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 // in the pool emits it and starts its next draw at once, so cycle walks of
 // different lengths do not hold the wave at the slowest lane.  Every walk
 // returns to the pool within the domain size (the cycle through j < n returns
-// to j), and every iteration advances an unfinished draw, so per * size
-// iterations bound the loop; the bound is a wave-uniform counter.
+// to j), and every iteration advances an unfinished draw, so (slice length)
+// * size iterations bound the loop; the loop counter is wave-uniform.
 template <int ROUNDS>
 __device__ __forceinline__ void walk_draws(const FeistelDomain& dom, const uint32_t* rks,
                                            uint32_t* bits, uint32_t total, uint32_t draws,
