@@ -4,7 +4,7 @@ times), checked on sampled rows the oracle computes one by one."""
 import numpy as np
 import pytest
 
-from gpu_common import desc_of, need_gpu, sample_rows, say, spec_of, torch
+from gpu_common import desc_of, need_gpu, rows_of, sample_rows, say, spec_of, torch
 from oracle import attention as o_att
 from oracle import geometry as o_geo
 from oracle import rope as o_rope
@@ -69,6 +69,45 @@ def test_workload_end_to_end(name):
         I = o_geo.row_sets(sp, h // G, np.array([q]))[0]
         want = o_att.attend_one(Qr[h, q], Kr[h // G, I], Vr[h // G, I], 1 / np.sqrt(w.D))
         worst = max(worst, float(np.abs(got[h, q] - want).max()))
+    say(f"  {len(rows)} sampled rows, max err {worst:.3e}")
+    assert worst <= 2e-2
+
+
+def test_longest_sequence_end_to_end():
+    """The longest supported sequence (RIS_MAX_N = 262,144 tokens) on the
+    Qwen2-1.5B layer shape, Stochastic 1% with 10 seeds (AUTO attention):
+    about 6.9e9 index entries, so CSR offsets exceed 2^32.  Sampled rows
+    against the oracle, and row_ptr consistent with the closed-form bounds."""
+    from synth import STOCHASTIC, Workload
+    ris = need_gpu()
+    w = Workload("qwen2_256k_stochastic", 12, 2, 128, 262144, "bf16", STOCHASTIC, 10_000, 10)
+    say(f"longest sequence: Hq={w.Hq} Hkv={w.Hkv} N={w.N} D={w.D}")
+    Q, K, V = gaussian_qkv(w.Hq, w.Hkv, w.N, w.D, seed=2)
+    Qb, Kb, Vb = to_bf16(Q), to_bf16(K), to_bf16(V)
+    del Q, K, V
+    qd, kd, vd = Qb.cuda(), Kb.cuda(), Vb.cuda()
+    sp = spec_of(w.mode, w.density_ppm, w.N, w.Hkv, w.n_seeds, w.seed, 0, 1)
+    rp_d, ci_d = ris.build_csr(desc_of(ris, sp), "cuda", use_bound=True)
+    out = torch.empty(w.Hq, w.N, w.D, dtype=torch.bfloat16, device="cuda")
+    ris.sparse_attn(qd, kd, vd, rp_d, ci_d, out, ris.attn_desc(qd, kd, out))
+    torch.cuda.synchronize()
+    rp = rp_d.cpu().numpy()
+    assert rp[-1] > 2**32
+    counts = np.diff(rp)
+    q = np.tile(np.arange(w.N), w.Hkv)
+    n, kk, _ = o_geo._pool_and_draws(sp, q)
+    assert rp[0] == 0 and np.all(counts >= kk) and np.all(counts <= np.minimum(n, w.n_seeds * kk))
+    rows = sample_rows(w.N, w.Hq, k_each=4, seed=3)
+    Qr, Kr, Vr = Qb.float().numpy(), Kb.float().numpy(), Vb.float().numpy()
+    G = w.Hq // w.Hkv
+    got = out.float().cpu().numpy()
+    worst = 0.0
+    for h, qq in rows:
+        I = o_geo.row_sets(sp, h // G, np.array([qq]))[0]
+        g_idx = rows_of(rp, ci_d, [(h // G) * w.N + qq])[0]
+        assert np.array_equal(g_idx, I), (h, qq)
+        want = o_att.attend_one(Qr[h, qq], Kr[h // G, I], Vr[h // G, I], 1 / np.sqrt(w.D))
+        worst = max(worst, float(np.abs(got[h, qq] - want).max()))
     say(f"  {len(rows)} sampled rows, max err {worst:.3e}")
     assert worst <= 2e-2
 
