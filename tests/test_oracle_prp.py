@@ -153,7 +153,7 @@ def test_three_successive_draws_are_jointly_uniform(n):
     assert ok, stat
 
 
-@pytest.mark.parametrize("n", [300, 4097, 65537])
+@pytest.mark.parametrize("n", [300, 4097, 65537, 262144])
 def test_draws_on_large_pools_are_jointly_uniform_in_bins(n):
     """On six-round widths: (P(j), P(j+1)) for j = 0 and 7 in 32 x 32 bins,
     and (P(0), P(1), P(2)) in 16^3 bins, over independent keys."""
