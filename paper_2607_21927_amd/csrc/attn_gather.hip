@@ -237,27 +237,10 @@ __global__ __launch_bounds__(64) void k_attn_gather(AttnParams a, float qscale) 
 //   * O += P V on MFMA with P packed to bf16 in registers and V staged
 //     row-major in the wave's LDS slice and read transposed.
 // ---------------------------------------------------------------------------
-typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
-typedef float f32x4_t __attribute__((ext_vector_type(4)));
-typedef float f32x2_t __attribute__((ext_vector_type(2)));
-typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
-typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
-typedef short s16x4_t __attribute__((ext_vector_type(4)));
-
 constexpr int kGWaves = 4;            // rows (waves) per workgroup
 constexpr int kGTile = 32;            // keys per tile
 constexpr float kGNegBig = -1e30f;    // finite start of the running max
 
-__device__ __forceinline__ uint2 lds_read_tr16(const uint16_t* ptr) {
-    typedef __attribute__((address_space(3))) s16x4_t lds_s16x4;
-    const s16x4_t v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(ptr));
-    return __builtin_bit_cast(uint2, v);
-}
-__device__ __forceinline__ bf16x8_t as_bf16x8(u32x4_t v) { return __builtin_bit_cast(bf16x8_t, v); }
-__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-    const f32x2_t f = {lo, hi};
-    return __builtin_bit_cast(uint32_t, __builtin_convertvector(f, bf16x2_t));
-}
 
 template <int D>
 struct GTile {

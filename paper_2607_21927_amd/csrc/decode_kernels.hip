@@ -29,33 +29,8 @@
 namespace ris {
 namespace {
 
-typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
-typedef float f32x4_t __attribute__((ext_vector_type(4)));
-typedef float f32x2_t __attribute__((ext_vector_type(2)));
-typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
-typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
-typedef short s16x4_t __attribute__((ext_vector_type(4)));
-
 constexpr int kTileKeys = kDecodeTileKeys;
 constexpr float kNegBig = -1e30f;   // finite start of the running max
-
-// LDS transpose read (ds_read_b64_tr_b16): within each group of 16 lanes,
-// lane i receives element i mod 4 of what lanes 4e + i/4 (e = 0..3) address.
-__device__ __forceinline__ uint2 lds_read_tr16(const uint16_t* ptr) {
-    typedef __attribute__((address_space(3))) s16x4_t lds_s16x4;
-    const s16x4_t v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(ptr));
-    return __builtin_bit_cast(uint2, v);
-}
-
-__device__ __forceinline__ bf16x8_t as_bf16x8(u32x4_t v) {
-    return __builtin_bit_cast(bf16x8_t, v);
-}
-
-// Two floats -> packed bf16 pair, round to nearest even (v_cvt_pk_bf16_f32).
-__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-    const f32x2_t f = {lo, hi};
-    return __builtin_bit_cast(uint32_t, __builtin_convertvector(f, bf16x2_t));
-}
 
 struct RowSegs {
     int64_t na, nw, ns;   // anchor entries, window keys, initial keys below the window

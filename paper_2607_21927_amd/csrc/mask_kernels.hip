@@ -61,7 +61,6 @@ __device__ __forceinline__ void split_draw(uint32_t idx, uint32_t draws, float i
     if (j >= (int)draws) { ++s; j -= (int)draws; }
 }
 
-typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 // One lane's share of the batch's (seed, draw) pairs, OR-ed into the bitmap.
 // Lane t takes the contiguous flat indices [t per, (t+1) per) (flat index =
