@@ -185,3 +185,36 @@ def test_binding_rejects_tensors_that_do_not_match_the_descriptor():
     with pytest.raises(ValueError):
         big = torch.zeros(Hq, N + 1, D, dtype=torch.bfloat16, device="cuda")
         ris.sparse_attn(big, k, k, rp, ci, out, d)                            # Q longer than N
+
+
+@pytest.mark.parametrize("algo", [1, 2, 0], ids=["gather", "tile", "auto"])
+def test_handmade_csr_with_empty_rows(algo):
+    """A CSR not produced by the geometry: every third row empty, the others
+    1-200 ascending keys anywhere in [0, N) (causal = 0), dense and sparse
+    32-row tiles mixed.  Empty rows yield zeros; the rest match the oracle."""
+    from oracle import attention as o_att
+    ris = need_gpu()
+    Hq, Hkv, N, D = 12, 2, 300, 128
+    rng = np.random.default_rng(11)
+    rows = []
+    for r in range(Hkv * N):
+        q = r % N
+        if q % 3 == 0:
+            rows.append(np.zeros(0, dtype=np.int32))
+        else:
+            n = int(rng.integers(1, 201)) if (q // 32) % 2 else int(rng.integers(1, 8))
+            rows.append(np.sort(rng.choice(N, size=n, replace=False)).astype(np.int32))
+    rp = np.zeros(Hkv * N + 1, dtype=np.int64)
+    rp[1:] = np.cumsum([len(x) for x in rows])
+    ci = np.concatenate(rows)
+    Q, K, V = gaussian_qkv(Hq, Hkv, N, D, seed=4)
+    Qb, Kb, Vb = to_bf16(Q), to_bf16(K), to_bf16(V)
+    qd, kd, vd = Qb.cuda(), Kb.cuda(), Vb.cuda()
+    out = torch.full((Hq, N, D), 7.0, dtype=torch.float32, device="cuda")
+    ris.sparse_attn(qd, kd, vd, torch.from_numpy(rp).cuda(), torch.from_numpy(ci).cuda(), out,
+                    ris.attn_desc(qd, kd, out, causal=0, algo=algo))
+    got = out.cpu().numpy()
+    want = o_att.sparse_attention(Qb.float().numpy(), Kb.float().numpy(), Vb.float().numpy(), rp, ci)
+    empty = np.arange(N) % 3 == 0
+    assert np.all(got[:, empty] == 0.0)
+    assert float(np.abs(got - want).max()) <= tight_tol(algo, float(np.abs(Vb.float().numpy()).max()))
