@@ -140,6 +140,19 @@ def _need_device(*ts):
             raise ValueError("tensors must be contiguous GPU tensors")
 
 
+def _capacity(col_idx, col_capacity):
+    """Entries the library may write: col_idx's size unless a smaller
+    capacity is given.  A capacity beyond the tensor would let the kernel
+    write past it, so it is refused here."""
+    if col_idx is None:
+        return 0
+    if col_capacity is None:
+        return col_idx.numel()
+    if col_capacity < 0 or col_capacity > col_idx.numel():
+        raise ValueError(f"col_capacity {col_capacity} outside [0, {col_idx.numel()}] (col_idx size)")
+    return int(col_capacity)
+
+
 def mask_desc(mode, density_ppm, N, heads, n_seeds=1, seed=0, layer=0, causal=1, block=0,
               window=0, anchor=0):
     return MaskDesc(mode, density_ppm, seed, n_seeds, layer, N, heads, causal, block, window,
@@ -161,7 +174,7 @@ def mask_build(desc, row_ptr, col_idx=None, col_capacity=None, stream=None):
         raise ValueError("row_ptr must be int64[heads*N + 1]")
     if col_idx is not None and col_idx.dtype != torch.int32:
         raise ValueError("col_idx must be int32")
-    cap = col_idx.numel() if (col_idx is not None and col_capacity is None) else (col_capacity or 0)
+    cap = _capacity(col_idx, col_capacity)
     _check(lib().ris_mask_build(ctypes.byref(desc), _ptr(row_ptr), _ptr(col_idx), cap,
                                 _stream(stream)), "ris_mask_build")
 
@@ -186,7 +199,7 @@ def mask_build_rows(desc, q_begin, q_count, row_ptr, col_idx=None, col_capacity=
     if col_idx is not None and (col_idx.dtype != torch.int32 or not col_idx.is_cuda
                                 or col_idx.stride(0) != 1):
         raise ValueError("col_idx must be a dense int32 GPU vector")
-    cap = col_idx.numel() if (col_idx is not None and col_capacity is None) else (col_capacity or 0)
+    cap = _capacity(col_idx, col_capacity)
     _check(lib().ris_mask_build_rows(ctypes.byref(desc), q_begin, q_count, _ptr(row_ptr),
                                      _ptr(col_idx), cap, _stream(stream)), "ris_mask_build_rows")
 
@@ -325,6 +338,10 @@ def build_csr(desc, device="cuda", stream=None, use_bound=False):
         cap = mask_nnz_bound(desc)
     else:
         mask_build(desc, row_ptr, None, stream=stream)
+        if stream is not None:
+            # The read-back below runs on torch's current stream; the count
+            # ran on the caller's, so wait for the device first.
+            torch.cuda.synchronize(row_ptr.device)
         cap = int(row_ptr[-1].item())
     col_idx = torch.empty(max(cap, 1), dtype=torch.int32, device=device)
     mask_build(desc, row_ptr, col_idx, col_capacity=cap, stream=stream)

@@ -212,3 +212,16 @@ def test_host_layer_validation(ris):
     assert L.ris_swiglu(f, None, 4, 8, 1, None) == -1
     assert L.ris_swiglu(f, f, 4, 0, 1, None) == -1
     assert L.ris_swiglu(f, f, 4, 8, 2, None) == -3
+
+
+def test_binding_refuses_capacity_beyond_col_idx(ris):
+    """A col_capacity larger than the col_idx tensor would let the kernel
+    write past it: the binding refuses it before any call."""
+    import torch
+    ci = torch.empty(10, dtype=torch.int32)
+    assert ris._capacity(None, None) == 0
+    assert ris._capacity(ci, None) == 10
+    assert ris._capacity(ci, 7) == 7
+    for bad in (11, -1):
+        with pytest.raises(ValueError):
+            ris._capacity(ci, bad)
