@@ -75,7 +75,8 @@ __device__ __forceinline__ void split_draw(uint32_t idx, uint32_t draws, float i
 // different lengths do not hold the wave at the slowest lane.  Every walk
 // returns to the pool within the domain size (the cycle through j < n returns
 // to j), and every iteration advances an unfinished draw, so (slice length)
-// * size iterations bound the loop; the loop counter is wave-uniform.
+// * size iterations bound the loop; the bound, from the longest slice, is
+// the same in every lane, so the counter lives in scalar registers.
 template <int ROUNDS>
 __device__ __forceinline__ void walk_draws(const FeistelDomain& dom, const uint32_t* rks,
                                            uint32_t* bits, uint32_t total, uint32_t draws,
@@ -85,9 +86,10 @@ __device__ __forceinline__ void walk_draws(const FeistelDomain& dom, const uint3
     const uint32_t hi = min(lo + per, total);
     if (lo >= hi) return;
     // Walker A takes the lane's draws from the front, walker B from the back;
-    // `rest` counts the draws neither has started.
+    // iA and iB are the flat indices they hold (iB = hi when B never starts),
+    // and a walker is done when its next index is the other's.
     bool actA = true, actB = hi - lo >= 2;
-    uint32_t rest = hi - lo - (actB ? 2u : 1u);
+    uint32_t iA = lo, iB = actB ? hi - 1u : hi;
     int sA = 0, jA = 0, sB = 0, jB = 0;
     split_draw(lo, draws, inv_draws, sA, jA);
     if (actB) split_draw(hi - 1, draws, inv_draws, sB, jB);
@@ -119,7 +121,8 @@ __device__ __forceinline__ void walk_draws(const FeistelDomain& dom, const uint3
     const u16x2_t sh_a = {(unsigned short)(16u - dom.a), (unsigned short)(16u - dom.a)};
     const u16x2_t sh_b = {(unsigned short)(16u - b), (unsigned short)(16u - b)};
     uint32_t xA = (uint32_t)jA, xB = (uint32_t)jB;
-    const uint64_t max_it = (uint64_t)(hi - lo) * dom.size;
+    // per >= hi - lo, and per and the domain size are the same in every lane.
+    const uint64_t max_it = (uint64_t)per * dom.size;
     for (uint64_t it = 0; it < max_it; ++it) {
         uint32_t L = (xA >> b) | ((xB >> b) << 16);
         uint32_t R = (xA & mb) | ((xB & mb) << 16);
@@ -129,10 +132,10 @@ __device__ __forceinline__ void walk_draws(const FeistelDomain& dom, const uint3
         xB = ((L >> 16) << b) | (R >> 16);
         if (actA && xA < n) {
             atomicOr(&bits[xA >> 5], 1u << (xA & 31u));
-            if (rest == 0u) {
+            if (iA + 1u == iB) {
                 actA = false;
             } else {
-                --rest;
+                ++iA;
                 if (++jA == (int)draws) {
                     jA = 0;
                     ++sA;
@@ -143,10 +146,10 @@ __device__ __forceinline__ void walk_draws(const FeistelDomain& dom, const uint3
         }
         if (actB && xB < n) {
             atomicOr(&bits[xB >> 5], 1u << (xB & 31u));
-            if (rest == 0u) {
+            if (iB - 1u == iA) {
                 actB = false;
             } else {
-                --rest;
+                --iB;
                 if (jB == 0) {
                     jB = (int)draws;
                     --sB;
