@@ -61,6 +61,22 @@ def test_mask_bound_sized_fill_and_determinism():
     assert torch.equal(rp2, rp3) and torch.equal(ci2, ci3)
 
 
+@pytest.mark.parametrize("use_bound", [False, True], ids=["exact", "bound"])
+def test_build_csr_on_a_side_stream(use_bound):
+    """Both phases on a caller's stream (not torch's current one), with the
+    count read back in between: the CSR equals the default-stream one."""
+    ris = need_gpu()
+    sp = spec_of(0, 20_000, 4000, 2, 10)
+    rp0, ci0 = gpu_csr(ris, sp)
+    side = torch.cuda.Stream()
+    say(f"side stream build_csr use_bound={use_bound}")
+    rp, ci = ris.build_csr(desc_of(ris, sp), "cuda", stream=side, use_bound=use_bound)
+    side.synchronize()
+    nnz = int(rp0[-1].item())
+    assert torch.equal(rp, rp0)
+    assert torch.equal(ci[:nnz], ci0[:nnz])
+
+
 @pytest.mark.parametrize("shift", [1, 2, 3])
 def test_mask_into_unaligned_buffer(shift):
     """col_idx starting 1-3 elements past a 16-byte boundary: the rows are
