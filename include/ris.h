@@ -36,7 +36,11 @@ typedef enum {
     RIS_E_DTYPE = -3,        /* unknown element type                         */
     RIS_E_CAPACITY = -4,     /* col_idx capacity below the number of entries */
     RIS_E_UNSUPPORTED = -5,  /* valid request outside what is implemented    */
-    RIS_E_HIP = -6           /* HIP runtime error                            */
+    RIS_E_HIP = -6,          /* HIP runtime error                            */
+    RIS_E_INCOMPLETE = -7    /* a one-pass geometry build reported an        */
+                             /* incomplete CSR (row_ptr[heads*N] < 0); the   */
+                             /* library's calls never return it, the caller  */
+                             /* that reads row_ptr does                      */
 } ris_status;
 
 typedef enum { RIS_STOCHASTIC = 0, RIS_STRUCTURAL = 1 } ris_mode;
@@ -111,6 +115,15 @@ typedef struct {
  * One-pass build (col_idx != NULL, col_capacity >= ris_mask_nnz_bound(desc)):
  *   row_ptr need not hold anything; the call writes both row_ptr and col_idx,
  *   generating every row once, fully asynchronously.  This is the fast path.
+ *   Each row finds its offset by waiting on its predecessors' sizes; that wait
+ *   is bounded (about 0.7 s, far beyond any healthy run).  A row that gives
+ *   up, or whose predecessors' offsets are unknown because one gave up, writes
+ *   no keys and -1 as its row_ptr entry, and row_ptr[heads*N] is then -1:
+ *   the CSR is incomplete and must not be used (rebuild it, e.g. in two
+ *   phases).  The call itself still returns RIS_OK, since it does not wait
+ *   for the device; check row_ptr[heads*N] >= 0 where it is read back.  The
+ *   environment variable RIS_DEBUG_LOOKBACK_SPINS=<polls> lowers the bound
+ *   (a test hook: 0 gives up at the first wait).
  * Fill phase (col_idx != NULL, smaller capacity): row_ptr must hold the
  *   count phase's output for the same descriptor; the call first reads
  *   row_ptr[heads*N] (synchronising the stream), returns RIS_E_CAPACITY,
@@ -228,7 +241,10 @@ typedef struct {
  * and Pre-Fusion Unified Softmax").  Q, out: device [Hq, N, D]; K, V: device
  * [Hkv, N, D]; contiguous.  row_ptr / col_idx: the CSR from ris_mask_build
  * with heads = Hkv and the same N (ascending rows, entries in [0, N)).
- * Accumulation is float32.  An empty row yields zeros.
+ * Accumulation is float32.  An empty row yields zeros, and so does a row
+ * whose offsets are negative (a one-pass build that reported itself
+ * incomplete; such a CSR is not a valid input, this only keeps every read
+ * inside the buffers).
  */
 int ris_sparse_attn(const void* Q, const void* K, const void* V, const int64_t* row_ptr,
                     const int32_t* col_idx, void* out, const ris_attn_desc* desc, void* stream);

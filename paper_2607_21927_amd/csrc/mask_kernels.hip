@@ -15,6 +15,7 @@
 // in descending q (their cost grows with q) so the heavy rows start first.
 #include "ris_device.h"
 #include "ris_internal.h"
+#include "lookback.h"
 
 namespace ris {
 namespace {
@@ -337,18 +338,16 @@ __global__ __launch_bounds__(kThreads) void k_mask_fill(MaskParams p, const int6
 // the closed-form bound.  Each workgroup takes a ticket -- rows are processed
 // in row order -- builds its row bitmap once, and finds its offset by a
 // decoupled look-back over its predecessors' status words, which live in
-// row_ptr itself: bits 61/62 flag "row size known" / "inclusive prefix
-// known".  A row publishes its size before looking back (64 predecessors per
-// step, one per lane), and a ticket is only
-// ever waited on by later tickets, whose workgroups started after it; so every
-// wait ends.  The spin is bounded anyway: past the bound the row is left
-// unwritten rather than risk a hang.  Status words are read and written with
-// relaxed agent-scope atomics: they carry the only data exchanged.
-constexpr int64_t kFlagAgg = 1ll << 61;
-constexpr int64_t kFlagInc = 1ll << 62;
-constexpr int64_t kValueMask = kFlagAgg - 1;
-constexpr uint32_t kSpinLimit = 1u << 24;
-
+// row_ptr itself (the protocol and its flags are in lookback.h).  A row
+// publishes its size before looking back (64 predecessors per step, one per
+// lane), and a ticket is only ever waited on by later tickets, whose
+// workgroups started after it; so every wait ends.  The wait is bounded
+// anyway (p.spin_limit polls): past the bound the row publishes poison and
+// writes nothing, any row whose look-back reaches a poisoned prefix does the
+// same, and k_strip_status makes the total row_ptr[R] negative, so that an
+// incomplete CSR is reported rather than used.  Status words are read and
+// written with relaxed agent-scope atomics: they carry the only data
+// exchanged.
 __device__ __forceinline__ int64_t status_load(const int64_t* p) {
     return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
@@ -385,38 +384,38 @@ __global__ __launch_bounds__(kThreads) void k_mask_fused(MaskParams p, int64_t* 
         // Wave-wide look-back: lane i reads the status of row j-1-i, so each
         // step covers 64 predecessors.  The step ends at the nearest row whose
         // inclusive prefix is known, once every row before it is ready.
+        namespace lb = lookback;
         const int lane = threadIdx.x;
-        if (lane == 0) status_store(&row_ptr[r + 1], kFlagAgg | count);
+        if (lane == 0) status_store(&row_ptr[r + 1], lb::aggregate(count));
         int64_t prefix = 0;
-        bool ok = true;
+        bool poisoned = false;
         uint32_t spins = 0;
         for (int64_t j = r; j > 0;) {
             const int64_t idx = j - lane;                       // row idx-1's status
-            const int64_t v = idx > 0 ? status_load(&row_ptr[idx]) : kFlagInc;
-            const uint64_t inc = __ballot((v & kFlagInc) != 0);
-            const uint64_t ready = __ballot((v & (kFlagInc | kFlagAgg)) != 0);
-            const int first = inc ? (int)__ffsll((unsigned long long)inc) - 1 : 64;
-            const uint64_t need = first >= 63 ? ~0ull : ((1ull << (first + 1)) - 1ull);
-            if ((ready & need) != need) {
-                if (++spins > kSpinLimit) { ok = false; break; }
+            const int64_t v = idx > 0 ? status_load(&row_ptr[idx]) : lb::inclusive(0, false);
+            const int first = lb::step_end(__ballot(lb::is_inclusive(v)), __ballot(lb::is_ready(v)));
+            if (first < 0) {
+                if (spins++ >= p.spin_limit) { poisoned = true; break; }
                 __builtin_amdgcn_s_sleep(1);
                 continue;
             }
             // Lanes before `first` hold single row counts (below 2^32); lane
-            // `first` holds an inclusive prefix.
-            int64_t part = (int64_t)wave_sum_u32(lane < first ? (uint32_t)(v & kValueMask) : 0u);
+            // `first` holds an inclusive prefix, or poison.
+            int64_t part = (int64_t)wave_sum_u32(lane < first ? (uint32_t)lb::value(v) : 0u);
             if (first < 64) {
                 const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, first);
                 const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)((uint64_t)v >> 32), first);
-                part += (int64_t)((((uint64_t)hi << 32) | lo) & (uint64_t)kValueMask);
+                const int64_t vf = (int64_t)(((uint64_t)hi << 32) | lo);
+                if (lb::is_poisoned(vf)) { poisoned = true; break; }
+                part += lb::value(vf);
             }
             prefix += part;
             if (first < 64) break;
             j -= 64;
         }
         if (lane == 0) {
-            status_store(&row_ptr[r + 1], kFlagInc | (prefix + count));
-            s_base = ok ? prefix : -1;
+            status_store(&row_ptr[r + 1], lb::inclusive(prefix + count, poisoned));
+            s_base = poisoned ? -1 : prefix;
         }
     }
     __syncthreads();
@@ -433,9 +432,30 @@ __global__ void k_fill_i64(int64_t* x, int64_t n, int64_t v) {
     if (i < n) x[i] = v;
 }
 
-__global__ void k_strip_status(int64_t* row_ptr, int64_t n) {
-    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i < n) row_ptr[i] &= kValueMask;
+// After the one-pass build: strip the status flags of row_ptr[1 .. R].  A
+// poisoned row's entry becomes -1; if any row is poisoned, row_ptr[R] becomes
+// -1 as well.  row_ptr[0] is 0 when this runs (the fused kernel's last ticket
+// restores it); here it counts finished workgroups (low 32 bits) and poisoned
+// ones (high bits), and the last workgroup to finish resets it to 0.
+__global__ __launch_bounds__(256) void k_strip_status(int64_t* row_ptr, int64_t R) {
+    const int64_t i = 1 + (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    bool poison = false;
+    if (i <= R) {
+        const int64_t v = row_ptr[i];
+        poison = lookback::is_poisoned(v);
+        row_ptr[i] = lookback::stripped(v);
+    }
+    const int any = __syncthreads_or(poison);
+    if (threadIdx.x == 0) {
+        const uint64_t add = 1ull | (any ? (1ull << 32) : 0ull);
+        const uint64_t old = __hip_atomic_fetch_add(reinterpret_cast<uint64_t*>(row_ptr), add,
+                                                    __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+        if ((old & 0xFFFFFFFFull) == (uint64_t)gridDim.x - 1) {
+            // every other workgroup has stripped its entries
+            if (((old + add) >> 32) != 0) status_store(&row_ptr[R], -1);
+            status_store(row_ptr, 0);
+        }
+    }
 }
 
 // In-place inclusive scan of row_ptr[1 .. R] (row sizes -> end offsets);
@@ -512,7 +532,8 @@ hipError_t launch_mask_fused(const MaskParams& p, int64_t* row_ptr, int32_t* col
                        row_ptr, col_idx, capacity);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k_strip_status, dim3(eb), dim3(256), 0, st, row_ptr, rows + 1);
+    const unsigned sb = (unsigned)((rows + 255) / 256);
+    hipLaunchKernelGGL(k_strip_status, dim3(sb), dim3(256), 0, st, row_ptr, rows);
     return hipGetLastError();
 }
 

@@ -2,6 +2,7 @@
 // kernel dispatch.  Nothing here allocates device memory or keeps state.
 #include <math.h>
 #include <stdint.h>
+#include <stdlib.h>
 
 #include "ris.h"
 #include "ris_device.h"
@@ -46,8 +47,23 @@ int32_t resolve_block(const ris_mask_desc* d) {
     return b < 1 ? 1 : (int32_t)b;
 }
 
+// Polls of a predecessor's status before a row of the one-pass build gives
+// up (about 0.7 s of waiting; every wait ends long before in a healthy run).
+// RIS_DEBUG_LOOKBACK_SPINS overrides it: a test hook that makes the give-up
+// path run (0 = give up at the first wait).
+uint32_t lookback_spin_limit() {
+    const char* s = getenv("RIS_DEBUG_LOOKBACK_SPINS");
+    if (s && *s) {
+        char* end = nullptr;
+        const unsigned long v = strtoul(s, &end, 10);
+        if (end && *end == '\0') return v > 0xFFFFFFFFul ? 0xFFFFFFFFu : (uint32_t)v;
+    }
+    return 1u << 24;
+}
+
 MaskParams make_params(const ris_mask_desc* d, int64_t q0, int64_t nq) {
     MaskParams p;
+    p.spin_limit = lookback_spin_limit();
     p.q0 = q0;
     p.nq = nq;
     p.seed = d->seed;
@@ -111,6 +127,7 @@ const char* ris_status_string(int status) {
         case RIS_E_CAPACITY: return "RIS_E_CAPACITY: col_idx capacity below nnz";
         case RIS_E_UNSUPPORTED: return "RIS_E_UNSUPPORTED: valid request outside what is implemented";
         case RIS_E_HIP: return "RIS_E_HIP: HIP runtime error";
+        case RIS_E_INCOMPLETE: return "RIS_E_INCOMPLETE: one-pass geometry build gave up (row_ptr total < 0)";
         default: return "unknown ris_status";
     }
 }

@@ -10,7 +10,7 @@ import os
 PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(PKG, "libris.so")
 
-OK, E_ARG, E_SHAPE, E_DTYPE, E_CAPACITY, E_UNSUPPORTED, E_HIP = 0, -1, -2, -3, -4, -5, -6
+OK, E_ARG, E_SHAPE, E_DTYPE, E_CAPACITY, E_UNSUPPORTED, E_HIP, E_INCOMPLETE = 0, -1, -2, -3, -4, -5, -6, -7
 STOCHASTIC, STRUCTURAL = 0, 1
 F32, BF16 = 0, 1
 ROPE_PLAIN, ROPE_LINEAR, ROPE_YARN = 0, 1, 2
@@ -325,11 +325,25 @@ def sparse_attn(Q, K, V, row_ptr, col_idx, out, desc, stream=None):
     return out
 
 
+def check_complete(row_ptr, stream=None):
+    """Read row_ptr's total back (one 8-byte copy, after the work queued on
+    `stream`) and raise RisError(E_INCOMPLETE) when the one-pass build
+    reported an incomplete CSR (a negative total); returns nnz."""
+    import torch
+    if stream is not None:
+        torch.cuda.synchronize(row_ptr.device)
+    nnz = int(row_ptr[-1].item())
+    if nnz < 0:
+        raise RisError(E_INCOMPLETE, "ris_mask_build")
+    return nnz
+
+
 def build_csr(desc, device="cuda", stream=None, use_bound=False):
     """Both phases of ris_mask_build; returns (row_ptr, col_idx) on the device.
 
-    use_bound sizes col_idx from the host-side bound (no read-back between
-    the phases); otherwise the exact nnz is read back (one 8-byte copy).
+    use_bound sizes col_idx from the host-side bound (one pass, then one
+    8-byte read-back of the total to check that the build is complete);
+    otherwise the exact nnz is read back between the count and fill phases.
     """
     import torch
     row_ptr = torch.empty(desc.heads * desc.N + 1, dtype=torch.int64, device=device)
@@ -345,4 +359,6 @@ def build_csr(desc, device="cuda", stream=None, use_bound=False):
         cap = int(row_ptr[-1].item())
     col_idx = torch.empty(max(cap, 1), dtype=torch.int32, device=device)
     mask_build(desc, row_ptr, col_idx, col_capacity=cap, stream=stream)
+    if use_bound:
+        check_complete(row_ptr, stream)
     return row_ptr, col_idx

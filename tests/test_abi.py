@@ -49,7 +49,7 @@ def test_library_exports_every_declared_symbol(ris):
 
 
 def test_status_strings_and_version(ris):
-    for code in (0, -1, -2, -3, -4, -5, -6):
+    for code in (0, -1, -2, -3, -4, -5, -6, -7):
         assert ris.status_string(code).startswith("RIS_")
     assert ris.status_string(123) == "unknown ris_status"
     assert ris.version() >> 16 == 2 and ris.version() & 0xFFFF >= 4

@@ -178,3 +178,52 @@ def test_union_size_matches_its_expectation(name):
     mean = w.Hkv * float((n * P).sum())
     sd = np.sqrt(w.Hkv * float((n * P * (1.0 - P)).sum()))
     assert abs(nnz - mean) < 5 * sd, (nnz, mean, sd)
+
+
+def test_lookback_give_up_is_reported(monkeypatch):
+    """The one-pass build's bounded wait, forced to give up from the host
+    (RIS_DEBUG_LOOKBACK_SPINS=0: a row that finds a predecessor not ready
+    gives up at once, so every kernel exits normally).  A row that gives up,
+    or whose look-back meets a poisoned prefix, writes no keys and -1 as its
+    entry; the total row_ptr[R] is then -1 and the binding's check raises.
+    Nothing is written past col_idx's capacity, and every row that was not
+    poisoned still holds exactly the oracle's keys at its offset.  A build
+    with the normal bound afterwards is exact."""
+    ris = need_gpu()
+    sp = spec_of(0, 10_000, 16384, 2, 3)
+    say("look-back give-up: N=16384 heads=2 S=3, spin limit 0")
+    want_rp, want_ci = o_geo.build_csr(sp)
+    d = desc_of(ris, sp)
+    cap = ris.mask_nnz_bound(d)
+    guard = 4096
+    R = sp.heads * sp.N
+    rp = torch.empty(R + 1, dtype=torch.int64, device="cuda")
+    ci = torch.full((cap + guard,), -7, dtype=torch.int32, device="cuda")
+    monkeypatch.setenv("RIS_DEBUG_LOOKBACK_SPINS", "0")
+    ris.mask_build(d, rp, ci, col_capacity=cap)
+    torch.cuda.synchronize()
+    monkeypatch.delenv("RIS_DEBUG_LOOKBACK_SPINS")
+    rp_h, ci_h = rp.cpu().numpy(), ci.cpu().numpy()
+    assert (ci_h[cap:] == -7).all(), "write past the capacity"
+    counts = np.diff(want_rp)
+    poisoned = np.flatnonzero(rp_h[1:] < 0)
+    say(f"  total {rp_h[-1]}, {len(poisoned)} of {R} rows poisoned")
+    if rp_h[-1] >= 0:
+        # no row had to wait: the build is complete and exact
+        assert len(poisoned) == 0
+        assert np.array_equal(rp_h, want_rp) and np.array_equal(ci_h[: rp_h[-1]], want_ci)
+    else:
+        assert len(poisoned) > 0
+        with pytest.raises(ris.RisError) as e:
+            ris.check_complete(rp)
+        assert e.value.status == ris.E_INCOMPLETE
+        good = np.flatnonzero(rp_h[1:R] >= 0)          # rows 0 .. R-2 not poisoned
+        assert len(good) > 0
+        ends = rp_h[1:][good]
+        assert np.array_equal(ends, want_rp[1:][good]), "a row that was not poisoned has a wrong offset"
+        for i in range(0, len(good), max(1, len(good) // 200)):
+            r, e = good[i], ends[i]
+            assert np.array_equal(ci_h[e - counts[r]:e], want_ci[want_rp[r]:want_rp[r + 1]]), r
+    rp2, ci2 = gpu_csr(ris, sp, use_bound=True)
+    assert np.array_equal(rp2.cpu().numpy(), want_rp)
+    assert np.array_equal(ci2.cpu().numpy()[: want_rp[-1]], want_ci)
