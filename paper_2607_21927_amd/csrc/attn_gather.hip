@@ -93,8 +93,9 @@ __global__ __launch_bounds__(64) void k_attn_gather(AttnParams a, float qscale) 
     const int g = (int)(i % a.Hkv);
     if (tile_is_dense(a, g, q - q % kTileRows)) return;   // that tile runs on the tiled kernel
     const int64_t r = (int64_t)g * N + q;
-    const int64_t start = a.row_ptr[r];
-    const int64_t L = a.row_ptr[r + 1] - start;
+    int64_t start = a.row_ptr[r];
+    int64_t L = a.row_ptr[r + 1] - start;
+    if (start < 0 || L < 0) { start = 0; L = 0; }   // an incomplete build's rows: empty
 
     for (int e = lane; e < G * D; e += 64) {
         const int hh = e / D, d = e - hh * D;
@@ -154,8 +155,12 @@ __global__ __launch_bounds__(64) void k_attn_gather(AttnParams a, float qscale) 
             if (hh < G) {
                 const float sv = valid ? s[hh] : -INFINITY;
                 const float mn = fmaxf(m[hh], wave_max(sv));
-                const float corr = exp2f(m[hh] - mn);
-                const float p = exp2f(sv - mn);
+                // No valid entry yet (every index so far outside [0, N)): the
+                // reference stays -inf, and a finite stand-in keeps corr and p
+                // at 0 instead of exp2(-inf - -inf) = NaN.
+                const float mc = mn == -INFINITY ? 0.f : mn;
+                const float corr = exp2f(m[hh] - mc);
+                const float p = exp2f(sv - mc);
                 l[hh] = l[hh] * corr + wave_sum(p);
 #pragma unroll
                 for (int e = 0; e < DPL; ++e) acc[hh][e] *= corr;
@@ -289,8 +294,9 @@ __global__ __launch_bounds__(64 * kGWaves, 2) void k_attn_gather16(AttnParams a,
     if (tile_is_dense(a, g, q - q % kTileRows)) return;   // that tile runs on the tiled kernel
     const int G = a.G;
     uint16_t* vw = vlds + wave * kGTile * VS;
-    const int64_t start = a.row_ptr[(int64_t)g * N + q];
-    const int64_t L = a.row_ptr[(int64_t)g * N + q + 1] - start;
+    int64_t start = a.row_ptr[(int64_t)g * N + q];
+    int64_t L = a.row_ptr[(int64_t)g * N + q + 1] - start;
+    if (start < 0 || L < 0) { start = 0; L = 0; }   // an incomplete build's rows: empty
     const int32_t* idx = a.col_idx + start;
     const uint16_t* Kg = static_cast<const uint16_t*>(a.K) + (int64_t)g * N * D;
     const uint16_t* Vg = static_cast<const uint16_t*>(a.V) + (int64_t)g * N * D;

@@ -91,6 +91,7 @@ __global__ __launch_bounds__(128 * G) void k_attn_tile16(AttnParams a, float c) 
         if (q < N) {
             s = a.row_ptr[g * N + q];
             L = a.row_ptr[g * N + q + 1] - s;
+            if (s < 0 || L < 0) { s = 0; L = 0; }   // an incomplete build's rows: empty
         }
         rstart_s[tid] = s;
         rlen_s[tid] = (int)L;

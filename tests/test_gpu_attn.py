@@ -242,3 +242,44 @@ def test_large_scores_stay_finite(algo):
     want_rp, want_ci = o_geo.build_csr(sp)
     want = o_att.sparse_attention(Qb.float().numpy(), Kb.float().numpy(), Vb.float().numpy(), want_rp, want_ci)
     assert float(np.abs(got - want).max()) <= tight_tol(algo, float(np.abs(Vb.float().numpy()).max()))
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_gather_ignores_indices_outside_the_sequence(dtype):
+    """The gather kernels skip CSR entries outside [0, N) instead of reading
+    through them.  Rows here start with more than a whole 64-entry chunk of
+    such entries (negative and >= N) before their real keys, so the first
+    chunk of the row holds no valid key at all: the running max must stay
+    finite-safe (no exp2(-inf - -inf) = NaN) and the output must equal the
+    oracle over the valid keys alone (float32: 1e-5; bf16: the derived bar)."""
+    from oracle import attention as o_att
+    ris = need_gpu()
+    Hq, Hkv, N, D = 6, 2, 200, 64
+    rng = np.random.default_rng(12)
+    rows, valid_rows = [], []
+    for r in range(Hkv * N):
+        keys = np.sort(rng.choice(N, size=int(rng.integers(1, 60)), replace=False)).astype(np.int32)
+        junk = np.concatenate([np.full(70, -5), np.full(int(rng.integers(0, 40)), N + 3)]).astype(np.int32)
+        rows.append(np.concatenate([junk, keys]) if r % 2 == 0 else keys)
+        valid_rows.append(keys)
+    rp = np.zeros(Hkv * N + 1, dtype=np.int64)
+    rp[1:] = np.cumsum([len(x) for x in rows])
+    ci = np.concatenate(rows)
+    vrp = np.zeros(Hkv * N + 1, dtype=np.int64)
+    vrp[1:] = np.cumsum([len(x) for x in valid_rows])
+    vci = np.concatenate(valid_rows)
+    Q, K, V = gaussian_qkv(Hq, Hkv, N, D, seed=5)
+    if dtype == "bf16":
+        Qt, Kt, Vt = to_bf16(Q), to_bf16(K), to_bf16(V)
+    else:
+        Qt, Kt, Vt = (torch.from_numpy(a) for a in (Q, K, V))
+    qd, kd, vd = Qt.cuda(), Kt.cuda(), Vt.cuda()
+    out = torch.empty((Hq, N, D), dtype=torch.float32, device="cuda")
+    ris.sparse_attn(qd, kd, vd, torch.from_numpy(rp).cuda(), torch.from_numpy(ci).cuda(), out,
+                    ris.attn_desc(qd, kd, out, causal=0, algo=ris.ATTN_GATHER))
+    got = out.cpu().numpy()
+    want = o_att.sparse_attention(Qt.float().numpy(), Kt.float().numpy(), Vt.float().numpy(), vrp, vci)
+    assert np.isfinite(got).all()
+    err = float(np.abs(got - want).max())
+    say(f"  out-of-range entries ({dtype}): max err {err:.3e}")
+    assert err <= (1e-5 if dtype == "f32" else tight_tol(1, float(np.abs(Vt.float().numpy()).max())))
