@@ -1,6 +1,12 @@
 """End-to-end hot path at the workloads' full sizes (RoPE -> geometry ->
 sparse attention, bf16 in / bf16 out, the launch configuration the benchmark
-times), checked on sampled rows the oracle computes one by one."""
+times), checked on sampled rows the oracle computes one by one.
+
+Bar on the sampled outputs, element by element: the kernels form exact bf16
+products with float32 sums and round the softmax weights to bf16 before the
+PV product (relative 2^-9 per weight, so at most 2^-9 max|V| on the output),
+and the output itself is rounded to bf16 (half an ulp: at most 2^-9 |out|):
+|got - want| <= 2^-9 max|V| + 2^-9 |want| + 2e-4."""
 import numpy as np
 import pytest
 
@@ -45,7 +51,7 @@ def test_workload_end_to_end(name):
     del Q, K, V
     sp, out = gpu_pipeline(ris, w, Qb, Kb, Vb, layer)
 
-    rows = sample_rows(w.N, w.Hq, k_each=6, seed=1)
+    rows = sample_rows(w.N, w.Hq, k_each=28, seed=1)
     qs = np.array(sorted({q for _, q in rows}))
     Kr = Kb.float().numpy()
     Vr = Vb.float().numpy()
@@ -64,13 +70,21 @@ def test_workload_end_to_end(name):
         Qr = Qb.float().numpy()
     G = w.Hq // w.Hkv
     got = out.float().cpu().numpy()
-    worst = 0.0
+    v_max = float(np.abs(Vr).max())
+    worst = worst_ratio = 0.0
+    sets = {}
     for h, q in rows:
-        I = o_geo.row_sets(sp, h // G, np.array([q]))[0]
+        if (h // G, q) not in sets:
+            sets[(h // G, q)] = o_geo.row_sets(sp, h // G, np.array([q]))[0]
+        I = sets[(h // G, q)]
         want = o_att.attend_one(Qr[h, q], Kr[h // G, I], Vr[h // G, I], 1 / np.sqrt(w.D))
-        worst = max(worst, float(np.abs(got[h, q] - want).max()))
-    say(f"  {len(rows)} sampled rows, max err {worst:.3e}")
+        err = np.abs(got[h, q] - want)
+        tol = 2.0**-9 * v_max + 2.0**-9 * np.abs(want) + 2e-4
+        worst = max(worst, float(err.max()))
+        worst_ratio = max(worst_ratio, float((err / tol).max()))
+    say(f"  {len(rows)} sampled rows, max err {worst:.3e}, max err / bar {worst_ratio:.3f}")
     assert worst <= 2e-2
+    assert worst_ratio <= 1.0
 
 
 def test_longest_sequence_end_to_end():
@@ -101,15 +115,19 @@ def test_longest_sequence_end_to_end():
     Qr, Kr, Vr = Qb.float().numpy(), Kb.float().numpy(), Vb.float().numpy()
     G = w.Hq // w.Hkv
     got = out.float().cpu().numpy()
-    worst = 0.0
+    v_max = float(np.abs(Vr).max())
+    worst = worst_ratio = 0.0
     for h, qq in rows:
         I = o_geo.row_sets(sp, h // G, np.array([qq]))[0]
         g_idx = rows_of(rp, ci_d, [(h // G) * w.N + qq])[0]
         assert np.array_equal(g_idx, I), (h, qq)
         want = o_att.attend_one(Qr[h, qq], Kr[h // G, I], Vr[h // G, I], 1 / np.sqrt(w.D))
-        worst = max(worst, float(np.abs(got[h, qq] - want).max()))
-    say(f"  {len(rows)} sampled rows, max err {worst:.3e}")
+        err = np.abs(got[h, qq] - want)
+        worst = max(worst, float(err.max()))
+        worst_ratio = max(worst_ratio, float((err / (2.0**-9 * v_max + 2.0**-9 * np.abs(want) + 2e-4)).max()))
+    say(f"  {len(rows)} sampled rows, max err {worst:.3e}, max err / bar {worst_ratio:.3f}")
     assert worst <= 2e-2
+    assert worst_ratio <= 1.0
 
 
 def test_needle_recall_structural_32k():
