@@ -2,15 +2,18 @@
 
 One step = one layer (or, with --all-layers, every layer of the workload back
 to back, each with its own geometry) of the hot path over resident synthetic
-inputs:
-restore Q and K from pristine copies (RoPE rotates in place), RoPE on Q and K,
-geometry (the CSR of the seed-ensemble union, built in one pass into a
-col_idx sized from the closed-form bound), sparse attention.  The
-default workload is the Qwen2-1.5B-shaped layer at N = 65,536 tokens, 1%
-density, 70 seeds, YaRN x2 -- the configuration the headline metric names.
+inputs: RoPE of the unrotated Q and K into the rotated buffers, geometry (the
+CSR of the seed-ensemble union, built in one pass into a col_idx sized from
+the closed-form bound), sparse attention.  The default workload is the
+Qwen2-1.5B-shaped layer at N = 65,536 tokens, 1% density, 70 seeds, YaRN x2 --
+the configuration the headline metric names; the default line also carries
+one sub-object per other configuration ("workloads": the tiny float32 case,
+the 32k Qwen2 layers, the TinyLlama layer over 22 layers, and the Structural
+workloads under the paper's own block rule).
 
-Prints ONE JSON line (see the fields below).  `value` is attended
-(query-head, key) pairs per second of whole step time.
+Prints ONE JSON line.  `value` is attended (query-head, key) pairs per second
+of whole step time; `roofline` is the attention kernel's (the dominant one):
+method flops per launch over its HIP-event time against the bf16 MFMA peak.
 """
 import argparse
 import json
@@ -64,7 +67,28 @@ def _cpu_rows(task):
     return pairs, time.perf_counter() - t0
 
 
-def cpu_baseline(w, layer, Q, K, V, workers, stride):
+def host_cores():
+    """Sockets, physical cores and logical CPUs of the host (lscpu), and the
+    physical cores this process may run on (its CPU affinity)."""
+    import subprocess
+    allowed = os.sched_getaffinity(0)
+    try:
+        out = subprocess.run(["lscpu", "-p=CPU,CORE,SOCKET"], capture_output=True, text=True,
+                             timeout=10).stdout
+        rows = [tuple(int(x) for x in ln.split(",")[:3]) for ln in out.splitlines()
+                if ln and ln[0].isdigit()]
+    except (OSError, ValueError, subprocess.SubprocessError):
+        rows = []
+    if not rows:
+        n = os.cpu_count() or 1
+        return {"sockets": None, "physical_cores": None, "logical_cpus": n,
+                "physical_cores_available": len(allowed)}
+    return {"sockets": len({sk for _, _, sk in rows}), "physical_cores": len({(sk, c) for _, c, sk in rows}),
+            "logical_cpus": len(rows),
+            "physical_cores_available": len({(sk, c) for cpu, c, sk in rows if cpu in allowed})}
+
+
+def cpu_baseline(w, layer, Q, K, V, workers, stride, host):
     """Oracle pairs/s over every `stride`-th query row of each KV head."""
     from oracle import geometry as o_geo
     from oracle import rope as o_rope
@@ -94,7 +118,9 @@ def cpu_baseline(w, layer, Q, K, V, workers, stride):
     return {"value": pairs / wall, "unit": "pairs/s", "cores": workers, "kind": "oracle",
             "sample": f"every {stride}th query row of each KV head ({len(qs) * w.Hkv} rows, "
                       f"{pairs} attended pairs), geometry + RoPE share + attention, "
-                      f"{wall:.1f} s wall on {workers} worker processes"}
+                      f"{wall:.1f} s wall on {workers} worker processes (one per physical core, "
+                      f"one BLAS thread each)",
+            "host": {**host, "workers": workers}}
 
 
 # ---------------------------------------------------------------------------
@@ -118,20 +144,41 @@ def stream_copy_gbs(torch, nbytes=1 << 30, reps=10):
     return gbs
 
 
-def run_gpu(w, layers, Q, K, V, steps, warmup, algo):
+def run_gpu(w, layers, steps, warmup, algo, seed=0):
+    """Time the hot-path step of workload w on the GPU.
+
+    A step = for each layer of `layers`: RoPE of the unrotated Q and K into the
+    rotated buffers (the inputs stay as they are, so every step starts from the
+    same data), the one-pass geometry into a col_idx sized from the
+    closed-form bound, and the sparse attention.  The Structural 32k workload
+    plants its needles on the rotated vectors (where the +3 sigma logit gain is
+    exact) once, before the timed loop; its step's RoPE pass rotates the
+    unrotated inputs into buffers of the same shape, and geometry and attention
+    run on the planted ones.  Inputs are resident in HBM; per-phase times come
+    from HIP events on the stream the library launches on."""
     import torch
     from paper_2607_21927_amd import ris
     from synth import to_bf16
     dev = torch.device("cuda:0")
-    q0, k0, v = to_bf16(Q).to(dev), to_bf16(K).to(dev), to_bf16(V).to(dev)
+    Q, K, V = gaussian_qkv(w.Hq, w.Hkv, w.N, w.D, seed=seed)
+    if w.dtype == "bf16":
+        q0, k0, v = (to_bf16(x).to(dev) for x in (Q, K, V))
+    else:
+        q0, k0, v = (torch.from_numpy(x).to(dev) for x in (Q, K, V))
+    del Q, K, V
+    rd = (ris.rope_desc(w.rope, w.rope_base, orig_max_pos=w.rope_orig, factor=w.rope_factor)
+          if w.rope != ROPE_NONE else None)
+    q_rot = k_rot = None
+    if rd is not None:
+        q_rot, k_rot = torch.empty_like(q0), torch.empty_like(k0)
+    q_att, k_att = (q_rot, k_rot) if rd is not None else (q0, k0)
     if w.needles:
-        # Needles are planted on rotated vectors; this workload's step then
-        # starts from the rotated, planted inputs and skips RoPE.
-        raise SystemExit("needle workload: run its parity test instead")
-    # RoPE reads the unrotated inputs and writes the rotated Q and K (the
-    # inputs stay as they are, so every step starts from the same data).
-    q, k = (torch.empty_like(q0), torch.empty_like(k0)) if w.rope != ROPE_NONE else (q0, k0)
-    out = torch.empty(w.Hq, w.N, w.D, dtype=torch.bfloat16, device=dev)
+        ris.rope_from(q0, q_rot, rd)
+        ris.rope_from(k0, k_rot, rd)
+        planted = plant_needles(q_rot.float().cpu().numpy(), k_rot.float().cpu().numpy(), needle_plan(w.N))
+        q_att, k_att = to_bf16(planted.astype(np.float32)).to(dev), k_rot.clone()
+        del planted
+    out = torch.empty(w.Hq, w.N, w.D, dtype=q0.dtype, device=dev)
     descs = [ris.mask_desc(w.mode, w.density_ppm, w.N, w.Hkv, n_seeds=w.n_seeds, seed=w.seed,
                            layer=layer, block=w.block, window=w.window, anchor=w.anchor)
              for layer in layers]
@@ -139,39 +186,33 @@ def run_gpu(w, layers, Q, K, V, steps, warmup, algo):
     cap = ris.mask_nnz_bound(descs[0])
     row_ptr = torch.empty(w.Hkv * w.N + 1, dtype=torch.int64, device=dev)
     col_idx = torch.empty(cap, dtype=torch.int32, device=dev)
-    rd = (ris.rope_desc(w.rope, w.rope_base, orig_max_pos=w.rope_orig, factor=w.rope_factor)
-          if w.rope != ROPE_NONE else None)
-    ad = ris.attn_desc(q, k, out, mode=w.mode, block=w.block, algo=algo)
+    ad = ris.attn_desc(q_att, k_att, out, mode=w.mode, block=w.block, algo=algo)
     nnz = [0] * len(descs)
 
     def step(stamps):
-        # One layer after another; with several layers each has its own
-        # geometry (the layer index enters the hash) over the same inputs.
         for i, desc in enumerate(descs):
             ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)] if stamps is not None else None
             if ev:
                 ev[0].record()
             if rd is not None:
-                ris.rope_from(q0, q, rd)
-                ris.rope_from(k0, k, rd)
+                ris.rope_from(q0, q_rot, rd)
+                ris.rope_from(k0, k_rot, rd)
             if ev:
                 ev[1].record()
             # col_idx sized from the closed-form bound: one call builds the CSR.
             ris.mask_build(desc, row_ptr, col_idx, col_capacity=cap)
             if ev:
                 ev[2].record()
-            ris.sparse_attn(q, k, v, row_ptr, col_idx, out, ad)
+            ris.sparse_attn(q_att, k_att, v, row_ptr, col_idx, out, ad)
             if ev:
                 ev[3].record()
                 stamps.append(ev)
-            if stamps is None and len(descs) > 1:
-                nnz[i] = int(row_ptr[-1].item())
+            if stamps is None:
+                nnz[i] = ris.check_complete(row_ptr)      # every layer's CSR complete
 
-    for _ in range(warmup):
+    for _ in range(max(1, warmup)):
         step(None)
     torch.cuda.synchronize()
-    if len(descs) == 1 or warmup == 0:
-        nnz = None
     t_rope = t_mask = t_attn = 0.0
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     stamps = []
@@ -185,20 +226,84 @@ def run_gpu(w, layers, Q, K, V, steps, warmup, algo):
         t_rope += e0.elapsed_time(e1)
         t_mask += e1.elapsed_time(e2)
         t_attn += e2.elapsed_time(e3)
-    if nnz is None:
-        if len(descs) == 1:
-            nnz = [int(row_ptr[-1].item())]
-        else:
-            raise SystemExit("several layers need at least one warm-up step (it records nnz)")
-    copy_gbs = stream_copy_gbs(torch)
-    return dict(copy_gbs=copy_gbs, ms_step=total_ms / steps, ms_rope=t_rope / steps, ms_mask=t_mask / steps,
-                ms_attn=t_attn / steps, nnz=sum(nnz), layers=len(descs))
+    if ris.check_complete(row_ptr) != nnz[-1]:
+        raise SystemExit("the geometry changed between steps")
+    del q0, k0, v, q_rot, k_rot, q_att, k_att, out, row_ptr, col_idx
+    torch.cuda.empty_cache()
+    return dict(ms_step=total_ms / steps, ms_rope=t_rope / steps, ms_mask=t_mask / steps,
+                ms_attn=t_attn / steps, nnz=sum(nnz), layers=len(descs), steps=steps)
+
+
+def attn_kernel_name(w, algo):
+    G = w.Hq // w.Hkv
+    if w.dtype != "bf16":
+        return f"k_attn_gather<{w.D}>"
+    return f"k_attn_gather16<{w.D}>" if algo == 1 else f"k_attn_tile16<{w.D}, {G}>"
+
+
+def attn_roofline(w, g, algo, traffic=None):
+    """Roofline of one attention launch (one layer), from the HIP-event time
+    of ris_sparse_attn averaged over the timed launches.
+
+    The tiled kernel (bf16, every tile above the dispatch threshold) runs the
+    score and PV contractions on MFMA and reads each 64-key K/V block once per
+    32 rows x G heads from LDS, so its bound is the matrix unit: `achieved` =
+    the method's flops (4 D per attended (query head, key) pair: QK^T and PV)
+    per second against the dense bf16 peak.  `issued_dense_frac` prices the
+    masked-dense work it issues over every touched block (all causal pairs);
+    `traffic` and `hbm_traffic_frac` are the HBM bytes per launch from the
+    committed rocprofv3 counters of this kernel source (null when none match);
+    `effective_kv_gbs` is the K/V bytes the method reads per second (2 D x 2 B
+    + 4 B per kv-pair), an effective rate, not an HBM one.
+    The float32 gather kernel is priced against HBM."""
+    G = w.Hq // w.Hkv
+    t = g["ms_attn"] / g["layers"] * 1e-3
+    kv = g["nnz"] / g["layers"]
+    if w.dtype == "bf16" and algo != 1:
+        flops = kv * G * 4 * w.D
+        dense = w.Hq * w.N * (w.N + 1) / 2 * 4 * w.D
+        return {"bound": "mfma", "kernel": attn_kernel_name(w, algo),
+                "achieved": flops / t / 1e12, "peak": MFMA_BF16_PEAK_TFS, "unit": "TFLOP/s",
+                "frac": flops / t / 1e12 / MFMA_BF16_PEAK_TFS, "traffic": traffic,
+                "flops_per_launch": flops, "issued_dense_flops_per_launch": dense,
+                "issued_dense_frac": dense / t / 1e12 / MFMA_BF16_PEAK_TFS,
+                "hbm_traffic_gbs": traffic / t / 1e9 if traffic else None,
+                "hbm_traffic_frac": traffic / t / 1e9 / HBM_PEAK_GBS if traffic else None,
+                "effective_kv_gbs": kv * KV_PAIR_BYTES[w.D] / t / 1e9}
+    per_pair = 2 * w.D * (2 if w.dtype == "bf16" else 4) + 4
+    achieved = kv * per_pair / t / 1e9
+    return {"bound": "hbm", "kernel": attn_kernel_name(w, algo), "achieved": achieved,
+            "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
+            "bytes_per_kv_pair": per_pair}
+
+
+def workload_record(w, g, algo, extra=None):
+    """Per-workload figures of one timed run (a sub-object of the JSON line)."""
+    G = w.Hq // w.Hkv
+    pairs = g["nnz"] * G
+    rec = {"workload": w.name, "Hq": w.Hq, "Hkv": w.Hkv, "head_dim": w.D, "N": w.N, "dtype": w.dtype,
+           "mode": "structural" if w.mode == STRUCTURAL else "stochastic",
+           "density": w.density_ppm / 1e6, "seeds": w.n_seeds, "block": w.block,
+           "rope": ["none", "plain", "linear", "yarn"][w.rope + 1], "needles": w.needles,
+           "layers": g["layers"], "steps": g["steps"],
+           "ms_step": g["ms_step"], "ms_attn": g["ms_attn"], "ms_geometry": g["ms_mask"], "ms_rope": g["ms_rope"],
+           "ms_attn_per_layer": g["ms_attn"] / g["layers"],
+           "pairs_per_s": pairs / (g["ms_step"] * 1e-3), "attn_pairs_per_s": pairs / (g["ms_attn"] * 1e-3),
+           "kv_pairs": g["nnz"], "union_fraction": g["nnz"] / (g["layers"] * w.Hkv * w.N * (w.N + 1) / 2),
+           "roofline": attn_roofline(w, g, algo)}
+    if extra:
+        rec.update(extra)
+    return rec
 
 
 def kv_gather_figure(w, reps=5):
     """The gather kernel on the workload's own shape and density with a single
     seed (the union then stays below the tiled kernel's threshold, so every
-    row takes the per-row K/V gather): algorithmic K/V bytes per second."""
+    row takes the per-row K/V gather).  `effective_gbs` is algorithmic K/V
+    bytes per second; `llc_hbm_gbs` the bytes the committed counters of this
+    kernel source put past the L2 caches per second (served by the 256 MB
+    last-level cache and HBM together: per-head K/V of 33.6 MB fits the
+    last-level cache, and the counters do not split the two)."""
     import torch
     from paper_2607_21927_amd import ris
     dev = torch.device("cuda:0")
@@ -222,19 +327,26 @@ def kv_gather_figure(w, reps=5):
     e1.record()
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / reps
-    achieved = nnz * KV_PAIR_BYTES[w.D] / (ms * 1e-3) / 1e9
+    del q, k, v, rp, ci, out
+    torch.cuda.empty_cache()
+    effective = nnz * KV_PAIR_BYTES[w.D] / (ms * 1e-3) / 1e9
+    past_l2 = measured_traffic(f"attn_gather16_{w.name}_1seed", "paper_2607_21927_amd/csrc/attn_gather.hip")
     return {"kernel": f"k_attn_gather16<{w.D}>", "seeds": 1,
             "union_fraction": nnz / (w.Hkv * w.N * (w.N + 1) / 2), "kv_pairs": nnz, "ms": ms,
-            "achieved": achieved, "unit": "GB/s", "peak": HBM_PEAK_GBS, "frac": achieved / HBM_PEAK_GBS,
-            "bytes_per_kv_pair": KV_PAIR_BYTES[w.D]}
+            "effective_gbs": effective, "bytes_per_kv_pair": KV_PAIR_BYTES[w.D],
+            "llc_hbm_bytes_per_launch": past_l2,
+            "llc_hbm_gbs": past_l2 / (ms * 1e-3) / 1e9 if past_l2 else None,
+            "llc_hbm_frac_of_hbm_peak": past_l2 / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS if past_l2 else None}
 
 
-def measured_traffic(workload, kernel_source):
-    """HBM bytes per launch of the attention kernel from the committed
-    rocprofv3 counter record, or None when no record exists for this
-    workload or the kernel source changed since the counters were taken."""
+def measured_traffic(record, kernel_source):
+    """Bytes per launch past the L2 caches (FETCH_SIZE + WRITE_SIZE, each
+    scaled by its reading for a device copy of known size) from the committed
+    rocprofv3 counter record profiles/<record>_traffic.txt, or None when no
+    record exists or the kernel source changed since the counters were
+    taken."""
     import hashlib
-    path = os.path.join(PROFILES, f"attn_tile_{workload}_traffic.txt")
+    path = os.path.join(PROFILES, f"{record}_traffic.txt")
     if not os.path.exists(path):
         return None
     rec = dict(line.strip().split("=", 1) for line in open(path)
@@ -468,19 +580,32 @@ def run_model_bench(name, layers, steps, warmup):
     }
 
 
+# The configurations timed beside the headline one, one sub-object each in
+# the JSON line: the tiny float32 case, the 32k Qwen2 layers (Stochastic, and
+# Structural with needles), the TinyLlama layer over all 22 layers, and the
+# Structural workloads with the paper's own block rule.
+OTHER_WORKLOADS = [("tiny", False, 20), ("qwen2_32k_stochastic", False, 10),
+                   ("qwen2_32k_structural", False, 10), ("tinyllama_64k_structural", True, 3),
+                   ("qwen2_32k_structural_paper_block", False, 10),
+                   ("tinyllama_64k_structural_paper_block", False, 5)]
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=10)
-    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="qwen2_64k_stochastic_yarn", choices=sorted(WORKLOADS))
     ap.add_argument("--layer", type=int, default=0)
     ap.add_argument("--all-layers", action="store_true",
                     help="one step = every layer of the workload back to back (layer 0..L-1)")
     ap.add_argument("--algo", type=int, default=0, help="0 auto, 1 gather, 2 tile")
-    ap.add_argument("--cpu-workers", type=int, default=16)
+    ap.add_argument("--cpu-workers", type=int, default=16,
+                    help="most oracle worker processes (one per available physical core)")
     ap.add_argument("--cpu-stride", type=int, default=64)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--headline-only", action="store_true",
+                    help="time only the named workload (no per-configuration sub-objects)")
     ap.add_argument("--decode", action="store_true",
                     help="time the Hybrid-Anchor decode step instead of the prefill layer")
     ap.add_argument("--batch", type=int, default=32, help="sequences per decode step")
@@ -490,7 +615,7 @@ def main():
     ap.add_argument("--kv-gather", action="store_true",
                     help="time only the per-row K/V gather kernel (workload shape, one seed)")
     ap.add_argument("--no-kv-gather", action="store_true",
-                    help="leave the K/V gather figure out of the default line (profiling runs)")
+                    help="leave the K/V gather figure out of the line (profiling runs)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: the hot path needs no cross-GPU exchange and this "
@@ -502,17 +627,18 @@ def main():
     if args.kv_gather:
         w = WORKLOADS[args.workload]
         f = kv_gather_figure(w, reps=args.steps)
-        print(json.dumps({"metric": "K/V gather bandwidth (algorithmic bytes / kernel time)",
-                          "value": f["achieved"], "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
+        print(json.dumps({"metric": "K/V gather rate (algorithmic K/V bytes / kernel time)",
+                          "value": f["effective_gbs"], "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
                           "warmup": 2, "ms_per_step": f["ms"], "higher_is_better": True,
                           "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
                           "data": "synthetic: Gaussian Q/K/V (torch.randn, seed 1)",
                           "config": {"workload": w.name + "_1seed", "N": w.N, "Hq": w.Hq, "Hkv": w.Hkv,
                                      "head_dim": w.D, "density": w.density_ppm / 1e6, "seeds": 1},
-                          "roofline": {"bound": "hbm", "achieved": f["achieved"], "peak": HBM_PEAK_GBS,
-                                       "unit": "GB/s", "frac": f["frac"], "traffic": None,
-                                       "kernel": f["kernel"], "bytes_per_kv_pair": f["bytes_per_kv_pair"]},
-                          "kv_pairs": f["kv_pairs"], "union_fraction": f["union_fraction"]}))
+                          "roofline": {"bound": "hbm", "achieved": f["llc_hbm_gbs"], "peak": HBM_PEAK_GBS,
+                                       "unit": "GB/s", "frac": f["llc_hbm_frac_of_hbm_peak"],
+                                       "traffic": f["llc_hbm_bytes_per_launch"], "kernel": f["kernel"],
+                                       "note": "bytes past the L2 caches (last-level cache and HBM)"},
+                          "kv_gather": f}))
         return
     if args.decode:
         wl = args.workload if args.workload != "qwen2_64k_stochastic_yarn" else "qwen2_64k_full_geometry"
@@ -520,28 +646,35 @@ def main():
                                           not args.no_cpu_baseline)))
         return
     w = WORKLOADS[args.workload]
-    Q, K, V = gaussian_qkv(w.Hq, w.Hkv, w.N, w.D, seed=0)
 
     cpu = None
     if not args.no_cpu_baseline:
         # Before any GPU call: the worker pool forks this process.
-        workers = max(1, min(args.cpu_workers, os.cpu_count() or 1))
+        host = host_cores()
+        workers = max(1, min(args.cpu_workers, host["physical_cores_available"]))
         from synth import to_bf16
-        Qb, Kb, Vb = (to_bf16(x).float().numpy() for x in (Q, K, V))
-        cpu = cpu_baseline(w, args.layer, Qb, Kb, Vb, workers, args.cpu_stride)
+        Q, K, V = gaussian_qkv(w.Hq, w.Hkv, w.N, w.D, seed=0)
+        Qb, Kb, Vb = (to_bf16(x).float().numpy() for x in (Q, K, V)) if w.dtype == "bf16" else (Q, K, V)
+        del Q, K, V
+        cpu = cpu_baseline(w, args.layer, Qb, Kb, Vb, workers, args.cpu_stride, host)
         del Qb, Kb, Vb
+        print(f"bench: oracle baseline {cpu['value']:.3e} pairs/s on {workers} workers", file=sys.stderr,
+              flush=True)
 
     layers = list(range(w.layers)) if args.all_layers else [args.layer]
-    g = run_gpu(w, layers, Q, K, V, args.steps, args.warmup, args.algo)
+    g = run_gpu(w, layers, args.steps, args.warmup, args.algo)
+    print(f"bench: {w.name} {g['ms_step']:.3f} ms per step", file=sys.stderr, flush=True)
     G = w.Hq // w.Hkv
     pairs = g["nnz"] * G
-    causal_pairs = w.Hkv * w.N * (w.N + 1) / 2 * len(layers)
-    alg_bytes = g["nnz"] * KV_PAIR_BYTES[w.D]
-    achieved = alg_bytes / (g["ms_attn"] * 1e-3) / 1e9
     tiled = w.dtype == "bf16" and args.algo != 1
-    traffic = measured_traffic(w.name, "paper_2607_21927_amd/csrc/attn_tile.hip") if tiled else None
+    traffic = measured_traffic(f"attn_tile_{w.name}", "paper_2607_21927_amd/csrc/attn_tile.hip") if tiled else None
     gather = (kv_gather_figure(w) if w.dtype == "bf16" and not args.all_layers and not args.no_kv_gather
               else None)
+    rec = workload_record(w, g, args.algo)
+    import torch
+    copy_gbs = stream_copy_gbs(torch)
+    roof = attn_roofline(w, g, args.algo, traffic)
+    roof["measured_copy_gbs"] = copy_gbs
     res = {
         "metric": "attended (q,k) pairs/s (whole hot-path step: RoPE + geometry + attention)",
         "value": pairs / (g["ms_step"] * 1e-3),
@@ -553,13 +686,11 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16",
+        "dtype": "bf16" if w.dtype == "bf16" else "f32",
         "data": "synthetic: Gaussian Q/K/V (numpy default_rng(0)) at the layer shape",
         "config": {"workload": w.name, "Hq": w.Hq, "Hkv": w.Hkv, "head_dim": w.D, "N": w.N,
-                   "mode": "structural" if w.mode == STRUCTURAL else "stochastic",
-                   "density": w.density_ppm / 1e6, "seeds": w.n_seeds, "block": w.block,
-                   "window": w.window, "anchor": w.anchor,
-                   "rope": ["none", "plain", "linear", "yarn"][w.rope + 1],
+                   "mode": rec["mode"], "density": w.density_ppm / 1e6, "seeds": w.n_seeds, "block": w.block,
+                   "window": w.window, "anchor": w.anchor, "rope": rec["rope"],
                    **({"layers": f"0..{len(layers) - 1}"} if len(layers) > 1 else {"layer": args.layer})},
         "ms_per_layer_attn": g["ms_attn"] / len(layers),
         "ms_attn": g["ms_attn"],
@@ -567,29 +698,38 @@ def main():
         "ms_rope": g["ms_rope"],
         "attn_pairs_per_s": pairs / (g["ms_attn"] * 1e-3),
         "kv_pairs": g["nnz"],
-        "union_fraction": g["nnz"] / causal_pairs,
-        "hbm_gbs_attn": achieved,
-        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
-                     "kernel": (f"k_attn_tile16<{w.D}, {G}>" if tiled else
-                                f"k_attn_gather16<{w.D}>" if w.dtype == "bf16" else f"k_attn_gather<{w.D}>"),
-                     "measured_copy_gbs": g["copy_gbs"], "frac_of_measured_copy": achieved / g["copy_gbs"],
-                     "bytes_per_kv_pair": KV_PAIR_BYTES[w.D]},
-        # The tiled kernel reads each K/V block once per 32 rows, so its real
-        # bound is matrix/vector work: the method's flops (4 D G per kv-pair:
-        # QK^T and PV for the G heads) against the dense bf16 MFMA peak, and
-        # the masked-dense flops it actually issues over every touched block.
-        "roofline_mfma": {
-            "bound": "mfma", "unit": "TFLOP/s", "peak": MFMA_BF16_PEAK_TFS,
-            "achieved": pairs * 4 * w.D / (g["ms_attn"] * 1e-3) / 1e12,
-            "frac": pairs * 4 * w.D / (g["ms_attn"] * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFS,
-            "issued_dense_masked_tflops": (w.Hq * causal_pairs / w.Hkv * 4 * w.D
-                                           / (g["ms_attn"] * 1e-3) / 1e12) if tiled else None},
+        "union_fraction": rec["union_fraction"],
+        "roofline": roof,
         # The per-row K/V gather path (sparse unions), on this shape with one seed.
         "kv_gather": gather,
         "cpu_baseline": cpu,
     }
+    if not args.headline_only and not args.all_layers and args.workload == "qwen2_64k_stochastic_yarn":
+        others = []
+        for name, all_layers, steps in OTHER_WORKLOADS:
+            wo = WORKLOADS[name]
+            lo = list(range(wo.layers)) if all_layers else [0]
+            go = run_gpu(wo, lo, steps, 1, 0)
+            print(f"bench: {name} {go['ms_step']:.3f} ms per step", file=sys.stderr, flush=True)
+            extra = {"block_resolved": block_of(wo)}
+            if wo.needles:
+                extra["needle_note"] = ("needles planted once on the rotated inputs before the timed loop; "
+                                        "the step's RoPE pass rotates the unrotated inputs into buffers of "
+                                        "the same shape")
+            others.append(workload_record(wo, go, 0, extra))
+        res["workloads"] = others
     print(json.dumps(res))
+
+
+def block_of(w):
+    """The Structural block size a workload resolves to (the paper's rule when
+    block = 0), for the record; None in Stochastic mode."""
+    if w.mode != STRUCTURAL:
+        return None
+    if w.block > 0:
+        return w.block
+    b_max = max(1, min(w.N, (w.density_ppm * w.N + 500_000) // 1_000_000))
+    return max(1, min(w.N // 10, b_max))
 
 
 if __name__ == "__main__":

@@ -69,6 +69,15 @@ WORKLOADS = {
     "qwen2_64k_full_geometry": Workload(
         "qwen2_64k_full_geometry", 12, 2, 128, 65536, "bf16", STOCHASTIC, 10_000, 70,
         rope=ROPE_YARN, rope_base=1e6, rope_orig=32768, window=1024, anchor=4),
+    # The Structural workloads with the paper's own block rule,
+    # B = min(floor(N / 10), round(d N)): B = 328 at 32k / 1%, 3,277 at
+    # 64k / 5% (one layer).
+    "qwen2_32k_structural_paper_block": Workload(
+        "qwen2_32k_structural_paper_block", 12, 2, 128, 32768, "bf16", STRUCTURAL, 10_000, 10,
+        block=0, rope=ROPE_PLAIN, rope_base=1e6, rope_orig=32768),
+    "tinyllama_64k_structural_paper_block": Workload(
+        "tinyllama_64k_structural_paper_block", 32, 4, 64, 65536, "bf16", STRUCTURAL, 50_000, 10,
+        block=0),
 }
 
 
