@@ -5,10 +5,17 @@ float32 library GEMMs (contraction length K <= 640 here), so a layer's
 outputs move by at most about K float32 ulps (640 x 2^-24 ~ 4e-5 relative)
 of their inputs, and the final RMSNorm'd states (values of order 1, below 5)
 stay within 5e-5 of the float64 oracle.
-bfloat16: activations are rounded to bf16 between every step (relative
-2^-9 each, about 20 roundings per layer), so the bound is looser: 0.15
-absolute on order-1 outputs over two layers, plus agreement in direction
-(cosine > 0.999).
+bfloat16: each layer rounds its activations to bf16 R = 13 times on the way
+from its input to its output (the normed input, the QKV projection, the
+rotated Q and K, the softmax weights, the attention output, the O
+projection, the residual sum, the second norm, the gate/up projection, the
+SwiGLU product, the down projection, the second residual sum, the next
+norm), each a relative error of at most u = 2^-9.  Independent roundings add
+in quadrature, so over L layers the relative error of the final states is of
+order sqrt(R L) u; the bars allow twice that: ||got - want|| / ||want|| <=
+2 sqrt(R L) u and max |got - want| <= 2 sqrt(R L) u max|want| (0.020 and
+about 0.09 for the two-layer stacks here, against measured 0.008 and 0.045),
+plus agreement in direction (cosine > 0.999).
 """
 
 import numpy as np
@@ -60,10 +67,16 @@ def test_model_prefill_float32_matches_oracle(case):
 @pytest.mark.parametrize("case", CASES[:1] + CASES[2:3])
 def test_model_prefill_bf16_close_to_oracle(case):
     got, want = run(case, torch.bfloat16)
+    layers = MODELS[case[0]].layers
+    bound = 2.0 * np.sqrt(13 * layers) * 2.0**-9
     err = float(np.abs(got - want).max())
+    rel = float(np.linalg.norm(got - want) / np.linalg.norm(want))
     cos = float((got * want).sum() / (np.linalg.norm(got) * np.linalg.norm(want)))
-    say(f"  bf16 max err {err:.3e}, cosine {cos:.6f}")
-    assert np.isfinite(got).all() and err <= 0.15 and cos > 0.999
+    say(f"  bf16 max err {err:.3e} (bar {bound * np.abs(want).max():.3e}), relative L2 {rel:.3e} "
+        f"(bar {bound:.3e}), cosine {cos:.6f}")
+    assert np.isfinite(got).all() and cos > 0.999
+    assert rel <= bound
+    assert err <= bound * float(np.abs(want).max())
 
 
 def test_host_layers_match_closed_forms():
