@@ -303,6 +303,25 @@ int ris_decode_attn(const void* Q, const void* K, const void* V, const int64_t* 
                     void* workspace, int64_t workspace_bytes, const ris_decode_desc* desc,
                     void* stream);
 
+/*
+ * ris_decode_attn for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * the same step, with no workspace argument.  The partials live in a
+ * library-owned device array of RIS_DECODE_STATIC_BYTES per GPU, created
+ * with the library's code on that GPU and held until the process ends; the
+ * call itself allocates nothing.  Returns RIS_E_CAPACITY, launching nothing,
+ * when ris_decode_workspace_bytes(desc) exceeds RIS_DECODE_STATIC_BYTES.
+ * Every call on one GPU uses that GPU's one array: calls that may overlap in
+ * time on the same GPU (unordered streams, several host threads) race on it
+ * and must not be made; calls ordered on one stream are safe.  Its contents
+ * need no initialisation (every partial is written before it is read).
+ * Arguments and results otherwise as ris_decode_attn.
+ */
+#define RIS_DECODE_STATIC_BYTES (32ll << 20)
+int ris_decode_attn_static(const void* Q, const void* K, const void* V, const int64_t* pos,
+                           const int64_t* anchor_ptr, const int32_t* anchor_idx, void* out,
+                           const ris_decode_desc* desc, void* stream);
+
 /* ------------------------------------------------------------------------ */
 /* Host-model layers for a model-level prefill                               */
 /* ------------------------------------------------------------------------ */

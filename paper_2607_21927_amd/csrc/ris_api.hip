@@ -4,6 +4,8 @@
 #include <stdint.h>
 #include <stdlib.h>
 
+#include <atomic>
+
 #include "ris.h"
 #include "ris_device.h"
 #include "ris_internal.h"
@@ -341,6 +343,49 @@ int64_t ris_decode_workspace_bytes(const ris_decode_desc* desc) {
     const int st = validate_decode(desc);
     if (st != RIS_OK) return st;
     return decode_workspace(*desc);
+}
+
+}  // extern "C"
+
+// ---- decode step without a caller workspace
+
+namespace {
+
+// The partials of ris_decode_attn_static: a file-scope device array, one copy
+// per GPU, alive until the process ends.  Host code never passes the array's
+// name to a kernel (on the host it is only a stand-in); it passes the device
+// address hipGetSymbolAddress gives on the current device.
+constexpr int64_t kDecodeStaticBytes = RIS_DECODE_STATIC_BYTES;
+__device__ __align__(256) unsigned char scratch[kDecodeStaticBytes];
+
+constexpr int kMaxDevices = 64;
+std::atomic<void*> g_scratch_ptr[kMaxDevices];
+
+// Device address of the current device's copy of `scratch`, looked up once
+// per device (a lookup, no allocation); nullptr on failure.
+void* device_scratch() {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+    void* ptr = g_scratch_ptr[dev].load(std::memory_order_acquire);
+    if (ptr) return ptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) return nullptr;
+    g_scratch_ptr[dev].store(ptr, std::memory_order_release);
+    return ptr;
+}
+
+}  // namespace
+
+extern "C" {
+
+int ris_decode_attn_static(const void* Q, const void* K, const void* V, const int64_t* pos,
+                           const int64_t* anchor_ptr, const int32_t* anchor_idx, void* out,
+                           const ris_decode_desc* desc, void* stream) {
+    const int st = validate_decode(desc);
+    if (st != RIS_OK) return st;
+    if (decode_workspace(*desc) > kDecodeStaticBytes) return RIS_E_CAPACITY;
+    void* ws = device_scratch();
+    if (!ws) return RIS_E_HIP;
+    return ris_decode_attn(Q, K, V, pos, anchor_ptr, anchor_idx, out, ws, kDecodeStaticBytes, desc, stream);
 }
 
 int ris_decode_attn(const void* Q, const void* K, const void* V, const int64_t* pos,

@@ -81,6 +81,8 @@ def lib():
         L.ris_decode_attn.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, i64,
                                       ctypes.POINTER(DecodeDesc), vp]
         L.ris_decode_attn.restype = ctypes.c_int
+        L.ris_decode_attn_static.argtypes = [vp, vp, vp, vp, vp, vp, vp, ctypes.POINTER(DecodeDesc), vp]
+        L.ris_decode_attn_static.restype = ctypes.c_int
         L.ris_rope.argtypes = [vp, i32, i32, i64, i32, i64, ctypes.POINTER(RopeDesc), vp]
         L.ris_rope.restype = ctypes.c_int
         L.ris_rope_from.argtypes = [vp, i64, i64, vp, i32, i32, i64, i32, i64, ctypes.POINTER(RopeDesc), vp]
@@ -97,7 +99,8 @@ def lib():
 
 EXPORTS = ("ris_mask_build", "ris_mask_nnz_bound", "ris_mask_build_rows",
            "ris_mask_rows_nnz_bound", "ris_rope", "ris_rope_from", "ris_sparse_attn",
-           "ris_decode_workspace_bytes", "ris_decode_attn", "ris_rmsnorm", "ris_swiglu",
+           "ris_decode_workspace_bytes", "ris_decode_attn", "ris_decode_attn_static", "ris_rmsnorm",
+           "ris_swiglu",
            "ris_status_string", "ris_version")
 
 
@@ -242,6 +245,34 @@ def decode_attn(Q, K, V, pos, anchor_ptr, anchor_idx, out, workspace, desc, stre
     _check(lib().ris_decode_attn(_ptr(Q), _ptr(K), _ptr(V), _ptr(pos), _ptr(anchor_ptr),
                                  _ptr(anchor_idx), _ptr(out), _ptr(workspace), nbytes,
                                  ctypes.byref(desc), _stream(stream)), "ris_decode_attn")
+    return out
+
+
+DECODE_STATIC_BYTES = 32 << 20
+
+
+def decode_attn_static(Q, K, V, pos, anchor_ptr, anchor_idx, out, desc, stream=None):
+    """ris_decode_attn_static: the decode step with the library's static
+    per-GPU partials (no workspace; nothing is allocated).  Calls that may
+    overlap on one GPU race on that buffer."""
+    import torch
+    _need_device(Q, K, V, pos, anchor_ptr, anchor_idx, out)
+    if pos.dtype != torch.int64 or anchor_ptr.dtype != torch.int64 or anchor_idx.dtype != torch.int32:
+        raise TypeError("pos and anchor_ptr must be int64, anchor_idx int32")
+    if pos.numel() != desc.batch or anchor_ptr.numel() != desc.batch * (desc.Hkv + 1):
+        raise ValueError("pos must hold B entries and anchor_ptr B * (Hkv + 1)")
+    if anchor_idx.numel() < desc.batch * desc.anchor_stride:
+        raise ValueError("anchor_idx must hold B * anchor_stride entries")
+    if not (Q.dtype == K.dtype == V.dtype) or K.shape != V.shape:
+        raise TypeError("Q, K, V must share a dtype and K, V a shape")
+    if _dtype_code(Q) != desc.dtype_in or _dtype_code(out) != desc.dtype_out:
+        raise TypeError("Q and out dtypes must match the descriptor")
+    if (tuple(Q.shape) != (desc.batch, desc.Hq, desc.D) or tuple(out.shape) != tuple(Q.shape)
+            or tuple(K.shape) != (desc.batch, desc.Hkv, desc.max_len, desc.D)):
+        raise ValueError("Q and out must be [B, Hq, D] and K, V [B, Hkv, max_len, D] as in the descriptor")
+    _check(lib().ris_decode_attn_static(_ptr(Q), _ptr(K), _ptr(V), _ptr(pos), _ptr(anchor_ptr),
+                                        _ptr(anchor_idx), _ptr(out), ctypes.byref(desc), _stream(stream)),
+           "ris_decode_attn_static")
     return out
 
 

@@ -34,7 +34,8 @@ def test_header_declares_the_boundary():
     names = declared_functions()
     assert names == sorted(["ris_mask_build", "ris_mask_nnz_bound", "ris_mask_build_rows",
                             "ris_mask_rows_nnz_bound", "ris_rope", "ris_rope_from", "ris_sparse_attn",
-                            "ris_decode_workspace_bytes", "ris_decode_attn", "ris_rmsnorm",
+                            "ris_decode_workspace_bytes", "ris_decode_attn", "ris_decode_attn_static",
+                            "ris_rmsnorm",
                             "ris_swiglu", "ris_status_string", "ris_version"])
 
 
@@ -186,6 +187,7 @@ def test_decode_validation(ris, bad, code):
     assert L.ris_decode_workspace_bytes(ctypes.byref(d)) == code
     f = ctypes.c_void_p(0x1000)       # never dereferenced: validation fails first
     assert L.ris_decode_attn(f, f, f, f, f, f, f, f, 1 << 40, ctypes.byref(d), None) == code
+    assert L.ris_decode_attn_static(f, f, f, f, f, f, f, ctypes.byref(d), None) == code
 
 
 def test_decode_workspace_size_and_capacity_error(ris):
@@ -200,6 +202,18 @@ def test_decode_workspace_size_and_capacity_error(ris):
     need = ris.decode_workspace_bytes(d)
     assert L.ris_decode_attn(f, f, f, f, f, f, f, f, need - 1, ctypes.byref(d), None) == -4
     assert L.ris_decode_attn(f, f, f, f, f, None, f, f, need, ctypes.byref(d), None) == -1
+
+
+def test_static_decode_rejects_workspaces_beyond_its_buffer(ris):
+    """ris_decode_attn_static refuses, before any device call, a descriptor
+    whose partials exceed the library's static buffer (RIS_E_CAPACITY)."""
+    L = ris.lib()
+    f = ctypes.c_void_p(0x1000)
+    big = _decode(ris, batch=8000, Hq=16, Hkv=2, D=128, max_len=16, anchor_stride=0, window=16, sink=0)
+    assert ris.decode_workspace_bytes(big) > ris.DECODE_STATIC_BYTES
+    assert L.ris_decode_attn_static(f, f, f, f, f, f, f, ctypes.byref(big), None) == -4
+    text = open(HEADER).read()
+    assert f"#define RIS_DECODE_STATIC_BYTES ({ris.DECODE_STATIC_BYTES >> 20}ll << 20)" in text
 
 
 def test_host_layer_validation(ris):
