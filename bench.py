@@ -627,6 +627,8 @@ def main():
     if args.kv_gather:
         w = WORKLOADS[args.workload]
         f = kv_gather_figure(w, reps=args.steps)
+        import torch
+        f["measured_copy_gbs"] = stream_copy_gbs(torch)
         print(json.dumps({"metric": "K/V gather rate (algorithmic K/V bytes / kernel time)",
                           "value": f["effective_gbs"], "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
                           "warmup": 2, "ms_per_step": f["ms"], "higher_is_better": True,
