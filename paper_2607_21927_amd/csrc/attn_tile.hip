@@ -5,14 +5,16 @@
 // When a row's unified set covers a sizeable share of its keys (a 70-seed
 // ensemble at 1% reaches ~50%), the sets of 32 neighbouring rows together
 // touch nearly every key block, so the work is a dense contraction under a
-// mask.  For every 64-key block the workgroup
+// mask.  For every key block (kKeys keys: 96 at D = 128, 128 at D = 64, the
+// most that double-buffered K/V and a triple-buffered bias fit in LDS) the
+// workgroup
 //   1. stages K[g, block] and V[g, block] in LDS, row-major, once for all
 //      32 rows x G heads (double-buffered: block kb+1 is staged while block
 //      kb is computed, one workgroup barrier per block);
 //   2. turns each row's CSR entries that fall in the block into a score
-//      bias in LDS, 0 at the row's keys and -inf elsewhere (a window of 64
-//      entries from the row's cursor suffices, the rows being ascending and
-//      unique);
+//      bias in LDS, 0 at the row's keys and -inf elsewhere (windows of 64
+//      entries from the row's cursor, enough to cover kKeys entries, the
+//      rows being ascending and unique);
 //   3. per wave (head h, 16 rows): S^T = bias + K_blk Q^T on MFMA (16x16x32
 //      bf16; the bias is the initial accumulator, so masking costs no
 //      vector instructions), one online-softmax update per query over the
@@ -28,8 +30,8 @@
 // so rescales of O are rare.  Every index of a row's set enters one
 // normalisation (Pre-Fusion Unified Softmax; Methods, "Hybrid Anchor and
 // Pre-Fusion Unified Softmax").  In Structural mode the block clique is the
-// diagonal 64-key block: the dense local tile runs on MFMA in the same
-// softmax state as the sampled global keys.
+// diagonal key block: the dense local tile runs on MFMA in the same softmax
+// state as the sampled global keys.
 //
 // 2G waves of at most ~150 VGPRs sit three or four to a SIMD: the MFMA work
 // of one wave overlaps the softmax of another.
@@ -39,11 +41,14 @@
 namespace ris {
 namespace {
 
-constexpr int kKeys = 64;   // keys per block
 constexpr float kSlack = 8.0f;
 
-template <int D, int G>
+template <int D, int G, int kKeys>
 __global__ __launch_bounds__(128 * G) void k_attn_tile16(AttnParams a, float c) {
+    static_assert(kKeys % 32 == 0 && kKeys <= 128, "key blocks of 32-key steps, at most two CSR windows");
+    constexpr int KT = kKeys / 16;                   // 16-key tiles of a block
+    constexpr int KU = kKeys / 32;                   // 32-key steps of the PV product
+    constexpr int WN = (kKeys + 63) / 64;            // 64-entry CSR windows per row
     constexpr int NW = 2 * G;                        // waves: (head, row half)
     constexpr int NT = 64 * NW;
     constexpr int KS = D + 16;          // K row stride in LDS (bf16 elements)
@@ -152,7 +157,7 @@ __global__ __launch_bounds__(128 * G) void k_attn_tile16(AttnParams a, float c) 
 
     // ---- register staging of one block (K and V pieces, CSR windows)
     u32x4_t kreg[PPT], vreg[PPT];
-    int wreg[RPW];
+    int wreg[RPW][WN];
     auto load_kv = [&](int kb) {
         const int k0 = kb * kKeys;
 #pragma unroll
@@ -169,7 +174,9 @@ __global__ __launch_bounds__(128 * G) void k_attn_tile16(AttnParams a, float c) 
     auto load_windows = [&]() {
 #pragma unroll
         for (int i = 0; i < RPW; ++i)
-            wreg[i] = lane < rln[i] - cur[i] ? a.col_idx[rst[i] + cur[i] + lane] : -1;
+#pragma unroll
+            for (int x = 0; x < WN; ++x)
+                wreg[i][x] = lane + 64 * x < rln[i] - cur[i] ? a.col_idx[rst[i] + cur[i] + 64 * x + lane] : -1;
     };
 
     // Stage block kb (its K/V pieces are in kreg/vreg, its CSR windows in
@@ -197,11 +204,16 @@ __global__ __launch_bounds__(128 * G) void k_attn_tile16(AttnParams a, float c) 
             if (r < kTileRows) {
                 // the window starts at the row's first unconsumed entry, so every
                 // valid entry is >= k0i; empty lanes hold -1
-                const uint32_t d = (uint32_t)(wreg[i] - k0i);
-                const bool inb = d < lim;
-                const uint64_t bal = __ballot(inb);
-                if (inb) bias[r * BS + d] = 0.f;
-                cur[i] += __popcll(bal);
+                int taken = 0;
+#pragma unroll
+                for (int x = 0; x < WN; ++x) {
+                    const uint32_t d = (uint32_t)(wreg[i][x] - k0i);
+                    const bool inb = d < lim;
+                    const uint64_t bal = __ballot(inb);
+                    if (inb) bias[r * BS + d] = 0.f;
+                    taken += __popcll(bal);
+                }
+                cur[i] += taken;
             }
         }
     };
@@ -244,12 +256,12 @@ __global__ __launch_bounds__(128 * G) void k_attn_tile16(AttnParams a, float c) 
         b3 = b3n;
         {
             // Every block of the range is computed: at the union densities the
-            // tiled kernel takes, a 64-key block with no entry in any of the
+            // tiled kernel takes, a key block with no entry in any of the
             // 32 rows is rare, and a fully masked block adds exact zeros.
             // ---- S^T[key, query] = K_blk Q_h^T; st[kt][i] is key 16 kt + 4 (l/16) + i
-            f32x4_t st[4];
+            f32x4_t st[KT];
 #pragma unroll
-            for (int kt = 0; kt < 4; ++kt) {
+            for (int kt = 0; kt < KT; ++kt) {
                 st[kt] = *reinterpret_cast<const f32x4_t*>(&bias[qr * BS + 16 * kt + 4 * lg]);
 #pragma unroll
                 for (int ks = 0; ks < KSL; ++ks) {
@@ -261,7 +273,7 @@ __global__ __launch_bounds__(128 * G) void k_attn_tile16(AttnParams a, float c) 
             // ---- mask, one online-softmax step for this lane's query
             float mx = -INFINITY;
 #pragma unroll
-            for (int kt = 0; kt < 4; ++kt)
+            for (int kt = 0; kt < KT; ++kt)
 #pragma unroll
                 for (int i = 0; i < 4; ++i) mx = fmaxf(mx, st[kt][i]);
             // The reference max moves only when the block's max exceeds it by
@@ -273,7 +285,7 @@ __global__ __launch_bounds__(128 * G) void k_attn_tile16(AttnParams a, float c) 
             const float m_new = move ? mxc : m_run;
             const float mc = m_new == -INFINITY ? 0.f : m_new;
 #pragma unroll
-            for (int kt = 0; kt < 4; ++kt)
+            for (int kt = 0; kt < KT; ++kt)
 #pragma unroll
                 for (int i = 0; i < 4; ++i) st[kt][i] = __builtin_amdgcn_exp2f(fmaf(st[kt][i], c, -mc));
             if (__ballot(move) != 0ull) {
@@ -285,16 +297,16 @@ __global__ __launch_bounds__(128 * G) void k_attn_tile16(AttnParams a, float c) 
             m_run = m_new;
             // ---- P^T as the B operand: 32-key step u holds keys 32u + 4 (l/16) + i
             // (slots 0..3) and 32u + 16 + 4 (l/16) + i (slots 4..7)
-            u32x4_t pb[2];
+            u32x4_t pb[KU];
 #pragma unroll
-            for (int u = 0; u < 2; ++u)
+            for (int u = 0; u < KU; ++u)
                 pb[u] = u32x4_t{pack_bf16x2(st[2 * u][0], st[2 * u][1]), pack_bf16x2(st[2 * u][2], st[2 * u][3]),
                                 pack_bf16x2(st[2 * u + 1][0], st[2 * u + 1][1]),
                                 pack_bf16x2(st[2 * u + 1][2], st[2 * u + 1][3])};
             // ---- O^T[d, query] += V_blk^T P^T: lane l addresses key row l/4
             // (then 16 + l/4) of the step at dims 16 dt + 4 (l%4)
 #pragma unroll
-            for (int u = 0; u < 2; ++u) {
+            for (int u = 0; u < KU; ++u) {
                 const uint16_t* v_lo = &Vs[(32 * u + (lane >> 2)) * VS + 4 * (lane & 3)];
 #pragma unroll
                 for (int dt = 0; dt < DT; ++dt) {
@@ -335,7 +347,11 @@ template <int D, int G>
 hipError_t launch_d_g(const AttnParams& a, float c, hipStream_t st) {
     const int64_t tiles = (a.N + kTileRows - 1) / kTileRows;
     const dim3 grid((unsigned)(tiles * a.Hkv));
-    hipLaunchKernelGGL((k_attn_tile16<D, G>), grid, dim3(128 * G), 0, st, a, c);
+    // Larger blocks amortise the per-block work (barrier, max exchange, bias
+    // reset, loop overhead) over more keys: 128 keys at D = 64, and 96 at
+    // D = 128, where 128 would not fit LDS.
+    constexpr int kKeys = D == 64 ? 128 : 96;
+    hipLaunchKernelGGL((k_attn_tile16<D, G, kKeys>), grid, dim3(128 * G), 0, st, a, c);
     return hipGetLastError();
 }
 
