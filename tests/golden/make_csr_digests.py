@@ -48,6 +48,8 @@ GEOMETRIES = [
                                          heads=4, block=64)),
     ("tinyllama_64k_structural", 21, dict(mode=1, density_ppm=50_000, seed=0, n_seeds=10, N=65536,
                                           heads=4, block=64)),
+    ("qwen2_64k_full_geometry", 0, dict(mode=0, density_ppm=10_000, seed=0, n_seeds=70, N=65536, heads=2,
+                                        window=1024, anchor=4)),
 ]
 
 
@@ -93,10 +95,18 @@ def tasks(selected):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--workers", type=int, default=8)
-    ap.add_argument("--only", nargs="*", default=[], help="workload names (default: all)")
+    ap.add_argument("--only", nargs="*", default=[],
+                    help="workload names to (re)compute; the other entries of the file are kept")
     args = ap.parse_args()
     t0 = time.time()
     res = []
+    if args.only and os.path.exists(OUT):
+        for line in open(OUT):
+            if line.startswith("#") or not line.strip():
+                continue
+            f = line.split()
+            if f[0] not in args.only:
+                res.append((f[0], int(f[1]), int(f[2]), int(f[3]), int(f[4]), int(f[5]), f[6], f[7]))
     with mp.get_context("fork").Pool(args.workers) as pool:
         for i, r in enumerate(pool.imap_unordered(block_digest, tasks(args.only), chunksize=1)):
             res.append(r)
@@ -105,8 +115,8 @@ def main():
     res.sort(key=lambda r: ([g[0] for g in GEOMETRIES].index(r[0]), r[1], r[2], r[3]))
     with open(OUT, "w") as f:
         f.write("# Oracle digests of the full-size geometry CSR (oracle.geometry.row_sets).\n")
-        f.write("# Written by: python tests/golden/make_csr_digests.py --workers "
-                f"{args.workers}\n")
+        f.write("# Written by: python tests/golden/make_csr_digests.py --workers 8 (every geometry; "
+                "--only NAME recomputes one)\n")
         f.write("# Per KV head and block of query rows [q0, q1): entries, sha256 of the row sizes\n")
         f.write("# (little-endian int64) and sha256 of the keys row after row (little-endian int32).\n")
         f.write("# workload layer kv_head q0 q1 nnz sha256_sizes sha256_keys\n")

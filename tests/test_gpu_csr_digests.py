@@ -41,7 +41,8 @@ def test_full_size_csr_matches_oracle_digests(name, layer):
     fields = dict(next(g[2] for g in GEOMETRIES if g[0] == name and g[1] == layer))
     want = load_digests()[(name, layer)]
     sp = spec_of(fields["mode"], fields["density_ppm"], fields["N"], fields["heads"],
-                 fields["n_seeds"], fields["seed"], layer, 1, fields.get("block", 0))
+                 fields["n_seeds"], fields["seed"], layer, 1, fields.get("block", 0),
+                 fields.get("window", 0), fields.get("anchor", 0))
     say(f"full-size CSR digests {name} layer {layer}: {len(want)} blocks")
     rp_d, ci_d = gpu_csr(ris, sp, use_bound=True)
     rp = rp_d.cpu().numpy()

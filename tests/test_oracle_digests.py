@@ -31,7 +31,7 @@ def test_descriptor_is_the_workloads(name, layer):
     assert (fields["mode"], fields["density_ppm"], fields["seed"], fields["n_seeds"], fields["N"],
             fields["heads"], fields.get("block", 0)) == (w.mode, w.density_ppm, w.seed, w.n_seeds, w.N,
                                                          w.Hkv, w.block)
-    assert w.window == 0 and w.anchor == 0
+    assert (fields.get("window", 0), fields.get("anchor", 0)) == (w.window, w.anchor)
     assert 0 <= layer < w.layers
 
 
@@ -47,6 +47,10 @@ def test_digests_cover_every_row_within_bounds(digests, name, layer):
     lo, hi = kk.copy(), np.minimum(n, sp.n_seeds * kk)
     if sp.mode == o_geo.STRUCTURAL:
         lo, hi = lo + (q - start + 1), hi + (q - start + 1)
+    if sp.window or sp.anchor:
+        win, anc = np.minimum(sp.window, q + 1), np.minimum(sp.anchor, q + 1)
+        lo = np.maximum(lo, np.maximum(win, anc))
+        hi = np.minimum(hi + win + anc, q + 1)
     for (h, q0, q1), (nnz, _, _) in blocks.items():
         assert lo[q0:q1].sum() <= nnz <= hi[q0:q1].sum(), (h, q0)
 
