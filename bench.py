@@ -714,6 +714,12 @@ def main():
             go = run_gpu(wo, lo, steps, 1, 0)
             print(f"bench: {name} {go['ms_step']:.3f} ms per step", file=sys.stderr, flush=True)
             extra = {"block_resolved": block_of(wo)}
+            tr = measured_traffic(f"attn_tile_{wo.name}", "paper_2607_21927_amd/csrc/attn_tile.hip")
+            if tr:
+                t = go["ms_attn"] / go["layers"] * 1e-3
+                extra["attn_traffic_per_launch"] = {"bytes": tr, "gbs": tr / t / 1e9,
+                                                    "frac_of_hbm_peak": tr / t / 1e9 / HBM_PEAK_GBS,
+                                                    "note": "layer 0's counters (profiles/)"}
             if wo.needles:
                 extra["needle_note"] = ("needles planted once on the rotated inputs before the timed loop; "
                                         "the step's RoPE pass rotates the unrotated inputs into buffers of "
