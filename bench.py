@@ -238,7 +238,8 @@ def attn_kernel_name(w, algo):
     G = w.Hq // w.Hkv
     if w.dtype != "bf16":
         return f"k_attn_gather<{w.D}>"
-    return f"k_attn_gather16<{w.D}>" if algo == 1 else f"k_attn_tile16<{w.D}, {G}>"
+    # the tiled kernel's key-block size: 96 keys at D = 128, 128 at D = 64
+    return f"k_attn_gather16<{w.D}>" if algo == 1 else f"k_attn_tile16<{w.D}, {G}, {96 if w.D == 128 else 128}>"
 
 
 def attn_roofline(w, g, algo, traffic=None):
