@@ -193,3 +193,52 @@ def test_walk_needs_fewer_than_two_evaluations_per_draw():
             steps[bad] += 1
             y[bad] = prp.feistel(y[bad], np.broadcast_to(w, (int(bad.sum()), 8)), m)
         assert steps.mean() < 2.0
+
+
+def _subset_counts(n, k, trials, seed):
+    """How often each k-subset of [0, n) is the drawn set, over independent
+    keys (one draw per key, so the cells are a true multinomial)."""
+    from math import comb
+    x = _draws(n, k, trials, seed)
+    if n <= 62:
+        code = (np.int64(1) << x).sum(axis=1)
+    else:                                   # k = 2 on a larger pool
+        xs = np.sort(x, axis=1)
+        code = xs[:, 0] * n + xs[:, 1]
+    _, c = np.unique(code, return_counts=True)
+    obs = np.zeros(comb(n, k))
+    obs[:c.size] = c
+    return obs
+
+
+SUBSET_CASES = [(6, 3), (8, 4), (10, 5), (12, 6), (16, 4), (20, 3), (33, 2), (33, 3), (130, 2)]
+
+
+@pytest.mark.parametrize("n,k", SUBSET_CASES)
+def test_drawn_subsets_are_uniform(n, k):
+    """The reading of the paper's per-seed draw is an exact-k uniform draw
+    without replacement: every k-subset of the pool equally likely.  Tested
+    directly over all C(n, k) subsets (chi-square at the 1e-4 false-alarm
+    level), on 12-round widths and on a 6-round one (n = 130)."""
+    from math import comb
+    C = comb(n, k)
+    trials = max(30000, 40 * C)
+    obs = _subset_counts(n, k, trials, 5000 + n * 7 + k)
+    assert obs.sum() == trials
+    ok, stat = _chi2_ok(obs, trials / C, C - 1)
+    assert ok, stat
+
+
+@pytest.mark.parametrize("n,k,rounds", [(6, 3, 2), (8, 4, 2), (12, 6, 4), (16, 4, 4), (20, 3, 4),
+                                        (33, 2, 4), (130, 2, 2), (8, 4, 6), (12, 6, 6)])
+def test_the_subset_test_rejects_weaker_networks(monkeypatch, n, k, rounds):
+    """The subset test has the power to catch a weaker mix: the same network
+    with fewer rounds fails it -- 2 or 4 rounds anywhere, and 6 rounds on
+    the smallest pools, which is why pools below 8 bits take 12."""
+    from math import comb
+    monkeypatch.setattr(prp, "rounds", lambda m: rounds)
+    C = comb(n, k)
+    trials = max(30000, 40 * C)
+    obs = _subset_counts(n, k, trials, 5000 + n * 7 + k)
+    ok, stat = _chi2_ok(obs, trials / C, C - 1)
+    assert not ok, stat
