@@ -148,16 +148,20 @@ __global__ __launch_bounds__(128 * G) void k_attn_tile16(AttnParams a, float c) 
     int rln[RPW], cur[RPW];
 #pragma unroll
     for (int i = 0; i < RPW; ++i) {
+        // the wave's rows: uniform values, kept in scalar registers so that
+        // the window addresses are scalar arithmetic
         const int r = w + NW * i;
-        rst[i] = r < kTileRows ? rstart_s[r] : 0;
-        rln[i] = r < kTileRows ? rlen_s[r] : 0;
+        const int64_t st = r < kTileRows ? rstart_s[r] : 0;
+        rst[i] = (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)(st >> 32)) << 32) |
+                           (uint32_t)__builtin_amdgcn_readfirstlane((int)st));
+        rln[i] = __builtin_amdgcn_readfirstlane(r < kTileRows ? rlen_s[r] : 0);
         cur[i] = 0;
     }
     const int kb_lo = kb_range[0], kb_hi = kb_range[1];
 
     // ---- register staging of one block (K and V pieces, CSR windows)
     u32x4_t kreg[PPT], vreg[PPT];
-    int wreg[RPW][WN];
+    int wreg[RPW];
     auto load_kv = [&](int kb) {
         const int k0 = kb * kKeys;
 #pragma unroll
@@ -171,12 +175,13 @@ __global__ __launch_bounds__(128 * G) void k_attn_tile16(AttnParams a, float c) 
             }
         }
     };
+    // The first 64-entry window from each row's cursor is prefetched a block
+    // ahead; a block with more entries than that (only when the row's set
+    // is denser than 64 per kKeys keys) reads the rest when it is staged.
     auto load_windows = [&]() {
 #pragma unroll
         for (int i = 0; i < RPW; ++i)
-#pragma unroll
-            for (int x = 0; x < WN; ++x)
-                wreg[i][x] = lane + 64 * x < rln[i] - cur[i] ? a.col_idx[rst[i] + cur[i] + 64 * x + lane] : -1;
+            wreg[i] = lane < rln[i] - cur[i] ? (a.col_idx + (rst[i] + cur[i]))[lane] : -1;
     };
 
     // Stage block kb (its K/V pieces are in kreg/vreg, its CSR windows in
@@ -205,13 +210,19 @@ __global__ __launch_bounds__(128 * G) void k_attn_tile16(AttnParams a, float c) 
                 // the window starts at the row's first unconsumed entry, so every
                 // valid entry is >= k0i; empty lanes hold -1
                 int taken = 0;
+                int wv = wreg[i];
 #pragma unroll
                 for (int x = 0; x < WN; ++x) {
-                    const uint32_t d = (uint32_t)(wreg[i][x] - k0i);
+                    const uint32_t d = (uint32_t)(wv - k0i);
                     const bool inb = d < lim;
                     const uint64_t bal = __ballot(inb);
                     if (inb) bias[r * BS + d] = 0.f;
                     taken += __popcll(bal);
+                    // the rows are ascending: unless the whole window lay in
+                    // the block, the block's entries end inside it
+                    if (x + 1 == WN || bal != ~0ull) break;
+                    const int pos = cur[i] + taken + lane;
+                    wv = pos < rln[i] ? a.col_idx[rst[i] + pos] : -1;
                 }
                 cur[i] += taken;
             }
