@@ -103,6 +103,9 @@ def cpu_baseline(w, layer, Q, K, V, workers, stride, host):
         Qr[:, qs] = o_rope.apply(Q[:, qs], w.rope, w.rope_base, 0, s, w.rope_orig, positions=qs)
         # K is rotated once for all rows; charge the sample its share of it.
         t_rope = (time.perf_counter() - t0) * (len(qs) / w.N)
+    if w.needles and stride == 1:
+        # the same planted inputs as the GPU run (input synthesis, not timed)
+        Qr = plant_needles(Qr, Kr, needle_plan(w.N)).astype(np.float32)
     spec = o_geo.MaskSpec(mode=w.mode, density_ppm=w.density_ppm, seed=w.seed,
                           n_seeds=w.n_seeds, layer=layer, N=w.N, heads=w.Hkv, block=w.block,
                           window=w.window, anchor=w.anchor)
@@ -116,10 +119,11 @@ def cpu_baseline(w, layer, Q, K, V, workers, stride, host):
     wall = time.perf_counter() - t0 + t_rope
     pairs = sum(r[0] for r in res)
     return {"value": pairs / wall, "unit": "pairs/s", "cores": workers, "kind": "oracle",
-            "sample": f"every {stride}th query row of each KV head ({len(qs) * w.Hkv} rows, "
+            "sample": (f"every query row of each KV head ({len(qs) * w.Hkv} rows, " if stride == 1 else
+                       f"every {stride}th query row of each KV head ({len(qs) * w.Hkv} rows, ") + (
                       f"{pairs} attended pairs), geometry + RoPE share + attention, "
                       f"{wall:.1f} s wall on {workers} worker processes (one per physical core, "
-                      f"one BLAS thread each)",
+                      f"one BLAS thread each)"),
             "host": {**host, "workers": workers}}
 
 
@@ -585,6 +589,11 @@ def run_model_bench(name, layers, steps, warmup):
 # the JSON line: the tiny float32 case, the 32k Qwen2 layers (Stochastic, and
 # Structural with needles), the TinyLlama layer over all 22 layers, and the
 # Structural workloads with the paper's own block rule.
+# The oracle's own timing beside each: every row of the tiny and 32k
+# workloads, every 64th row (of layer 0) for the 64k ones.
+CPU_STRIDE = {"tiny": 1, "qwen2_32k_stochastic": 1, "qwen2_32k_structural": 1,
+              "tinyllama_64k_structural": 64, "qwen2_32k_structural_paper_block": 1,
+              "tinyllama_64k_structural_paper_block": 64}
 OTHER_WORKLOADS = [("tiny", False, 20), ("qwen2_32k_stochastic", False, 10),
                    ("qwen2_32k_structural", False, 10), ("tinyllama_64k_structural", True, 3),
                    ("qwen2_32k_structural_paper_block", False, 10),
@@ -650,19 +659,28 @@ def main():
         return
     w = WORKLOADS[args.workload]
 
-    cpu = None
+    with_others = not args.headline_only and not args.all_layers and args.workload == "qwen2_64k_stochastic_yarn"
+    cpu, cpu_others = None, {}
     if not args.no_cpu_baseline:
         # Before any GPU call: the worker pool forks this process.
         host = host_cores()
         workers = max(1, min(args.cpu_workers, host["physical_cores_available"]))
-        from synth import to_bf16
-        Q, K, V = gaussian_qkv(w.Hq, w.Hkv, w.N, w.D, seed=0)
-        Qb, Kb, Vb = (to_bf16(x).float().numpy() for x in (Q, K, V)) if w.dtype == "bf16" else (Q, K, V)
-        del Q, K, V
-        cpu = cpu_baseline(w, args.layer, Qb, Kb, Vb, workers, args.cpu_stride, host)
-        del Qb, Kb, Vb
-        print(f"bench: oracle baseline {cpu['value']:.3e} pairs/s on {workers} workers", file=sys.stderr,
-              flush=True)
+        todo = [(w, args.cpu_stride)] + ([(WORKLOADS[n], CPU_STRIDE[n]) for n, _, _ in OTHER_WORKLOADS]
+                                         if with_others else [])
+        for wc, stride in todo:
+            from synth import to_bf16
+            Q, K, V = gaussian_qkv(wc.Hq, wc.Hkv, wc.N, wc.D, seed=0)
+            Qb, Kb, Vb = ((to_bf16(x).float().numpy() for x in (Q, K, V)) if wc.dtype == "bf16"
+                          else (Q, K, V))
+            del Q, K, V
+            c = cpu_baseline(wc, args.layer if wc is w else 0, Qb, Kb, Vb, workers, stride, host)
+            del Qb, Kb, Vb
+            if wc is w:
+                cpu = c
+            else:
+                cpu_others[wc.name] = c
+            print(f"bench: oracle baseline {wc.name} {c['value']:.3e} pairs/s on {workers} workers",
+                  file=sys.stderr, flush=True)
 
     layers = list(range(w.layers)) if args.all_layers else [args.layer]
     g = run_gpu(w, layers, args.steps, args.warmup, args.algo)
@@ -707,7 +725,7 @@ def main():
         "kv_gather": gather,
         "cpu_baseline": cpu,
     }
-    if not args.headline_only and not args.all_layers and args.workload == "qwen2_64k_stochastic_yarn":
+    if with_others:
         others = []
         for name, all_layers, steps in OTHER_WORKLOADS:
             wo = WORKLOADS[name]
@@ -725,7 +743,9 @@ def main():
                 extra["needle_note"] = ("needles planted once on the rotated inputs before the timed loop; "
                                         "the step's RoPE pass rotates the unrotated inputs into buffers of "
                                         "the same shape")
-            others.append(workload_record(wo, go, 0, extra))
+            rec_o = workload_record(wo, go, 0, extra)
+            rec_o["cpu_baseline"] = cpu_others.get(name)
+            others.append(rec_o)
         res["workloads"] = others
     print(json.dumps(res))
 
