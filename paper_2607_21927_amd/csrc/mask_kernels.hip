@@ -9,10 +9,13 @@
 // without duplicates (the unique() merge; Methods, "Hybrid Anchor and
 // Pre-Fusion Unified Softmax").
 //
-// Count pass: popcount -> row size -> row_ptr[r + 1]; a single-workgroup
-// scan turns sizes into offsets.  Fill pass: regenerate the bitmap, then a
-// block-wide prefix over word popcounts places every key.  Rows are launched
-// in descending q (their cost grows with q) so the heavy rows start first.
+// Two-pass build: the count pass writes each row's size (popcount) to
+// row_ptr[r + 1], a single-workgroup scan turns sizes into offsets, and the
+// fill pass regenerates the bitmap and places every key by a block-wide prefix
+// over word popcounts; rows are launched in descending q (their cost grows
+// with q) so the heavy rows start first.  One-pass build (col_idx sized from
+// the closed-form bound): a persistent grid builds every bitmap once and
+// finds each row's offset by a decoupled look-back (see k_mask_fused).
 #include "ris_device.h"
 #include "ris_internal.h"
 #include "lookback.h"
@@ -22,6 +25,22 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kSeedBatch = 256;  // row words of this many seeds live in LDS at once
+// A lane's slice of a batch, ceil(seeds * draws / kThreads) draws, is then at
+// most one seed's draws long: it spans at most one seed boundary.
+static_assert(kSeedBatch <= kThreads, "a lane's slice of a batch must not exceed one seed's draws");
+
+// LDS words of the seed batch's row words: a batch never holds more than
+// min(n_seeds, kSeedBatch) seeds.
+__host__ __device__ __forceinline__ int64_t rks_words(const MaskParams& p) {
+    return (int64_t)(p.n_seeds < kSeedBatch ? p.n_seeds : kSeedBatch) * kRowWords;
+}
+
+// Bitmap words of the largest pool of the built rows: q0 + nq keys (causal)
+// or N.
+__host__ __device__ __forceinline__ int64_t bitmap_words(const MaskParams& p) {
+    const int64_t span = p.causal ? p.q0 + p.nq : p.N;
+    return (span + 31) / 32;
+}
 
 struct RowGeom {
     uint32_t pool;          // draw pool [0, pool)
@@ -164,6 +183,97 @@ __device__ __forceinline__ void walk_draws(const FeistelDomain& dom, const uint3
     }
 }
 
+// The same walk for domains of at most 16 bits (pools of at most 65536 keys,
+// fewer than 65536 draws per seed): both walkers' values share one register
+// X, A in the low and B in the high 16 bits, so the split into halves and the
+// recombination after the rounds are one or two packed instructions each.  J
+// holds the two walkers' draw indices within their seeds the same way.  rem
+// counts the lane's draws that neither walker has started: a walker that
+// finishes a draw takes the next one from its end if rem was positive, and
+// stops otherwise (rem may go below zero once both have stopped).  A lane's
+// slice spans at most one seed boundary (kSeedBatch <= kThreads): a walker
+// that crosses it moves into the other walker's seed and copies that walker's
+// round keys from the other half of KM and KX.  The set of draws and each
+// draw's walk are those of walk_draws, so the bitmap is identical.
+template <int ROUNDS>
+__device__ __forceinline__ void walk_draws16(const FeistelDomain& dom, const uint32_t* rks,
+                                             uint32_t* bits, uint32_t total, uint32_t draws,
+                                             float inv_draws) {
+    const uint32_t per = (total + kThreads - 1) / kThreads;
+    const uint32_t lo = threadIdx.x * per;
+    const uint32_t hi = min(lo + per, total);
+    if (lo >= hi) return;
+    bool actA = true, actB = hi - lo >= 2;
+    int rem = (int)(hi - lo) - (actB ? 2 : 1);
+    int sA = 0, jA = 0, sB = 0, jB = 0;
+    split_draw(lo, draws, inv_draws, sA, jA);
+    if (actB) split_draw(hi - 1, draws, inv_draws, sB, jB);
+    else { sB = sA; jB = jA; }
+    uint32_t KM[ROUNDS], KX[ROUNDS];
+#pragma unroll
+    for (int r = 0; r < ROUNDS; ++r) {
+        const uint32_t ka = r < kRowWords ? rks[sA * kRowWords + r] : (rks[sA * kRowWords + r - kRowWords] ^ kKeyTweak);
+        const uint32_t kb = r < kRowWords ? rks[sB * kRowWords + r] : (rks[sB * kRowWords + r - kRowWords] ^ kKeyTweak);
+        KM[r] = (kb & 0xFFFF0000u) | (ka >> 16) | 0x00010001u;
+        KX[r] = (kb << 16) | (ka & 0xFFFFu);
+    }
+    const uint32_t b = dom.b, mb = (1u << b) - 1u, n = dom.n;
+    const uint32_t mb2 = mb | (mb << 16);
+    const u16x2_t shx = {(unsigned short)b, (unsigned short)b};
+    const u16x2_t sh_a = {(unsigned short)(16u - dom.a), (unsigned short)(16u - dom.a)};
+    const u16x2_t sh_b = {(unsigned short)(16u - b), (unsigned short)(16u - b)};
+    uint32_t J = (uint32_t)jA | ((uint32_t)jB << 16);
+    uint32_t X = J;
+    const uint64_t max_it = (uint64_t)per * dom.size;
+    for (uint64_t it = 0; it < max_it; ++it) {
+        uint32_t L = as_u32(as_u16x2(X) >> shx);
+        uint32_t R = X & mb2;
+        asm("" : "+v"(L), "+v"(R));
+#pragma unroll
+        for (int r = 0; r < ROUNDS; ++r) feistel_round_x2(L, R, KM[r], KX[r], (r & 1) ? sh_b : sh_a);
+        X = as_u32(as_u16x2(L) << shx) | R;
+        if (actA && (X & 0xFFFFu) < n) {
+            uint32_t w = __builtin_amdgcn_ubfe(X, 5, 11);
+            asm("" : "+v"(w));
+            atomicOr(&bits[w], 1u << (X & 31u));
+            if (--rem < 0) {
+                actA = false;
+            } else {
+                ++J;
+                if ((J & 0xFFFFu) == draws) {
+                    J &= 0xFFFF0000u;
+#pragma unroll
+                    for (int r = 0; r < ROUNDS; ++r) {
+                        KM[r] = __builtin_amdgcn_perm(KM[r], KM[r], 0x03020302u);
+                        KX[r] = __builtin_amdgcn_perm(KX[r], KX[r], 0x03020302u);
+                    }
+                }
+                X = __builtin_amdgcn_perm(X, J, 0x07060100u);
+            }
+        }
+        if (actB && (X >> 16) < n) {
+            uint32_t w = X >> 21;
+            asm("" : "+v"(w));
+            atomicOr(&bits[w], 1u << ((X >> 16) & 31u));
+            if (--rem < 0) {
+                actB = false;
+            } else {
+                if (J < 0x10000u) {
+                    J |= draws << 16;
+#pragma unroll
+                    for (int r = 0; r < ROUNDS; ++r) {
+                        KM[r] = __builtin_amdgcn_perm(KM[r], KM[r], 0x01000100u);
+                        KX[r] = __builtin_amdgcn_perm(KX[r], KX[r], 0x01000100u);
+                    }
+                }
+                J -= 0x10000u;
+                X = __builtin_amdgcn_perm(J, X, 0x07060100u);
+            }
+        }
+        if (!actA && !actB) break;
+    }
+}
+
 // Bits [lo, hi) that fall in word w.
 __device__ __forceinline__ uint32_t range_bits(uint32_t w, uint32_t lo, uint32_t hi) {
     const uint32_t b0 = w * 32u, b1 = b0 + 32u;
@@ -208,10 +318,14 @@ __device__ void build_row_bitmap(const MaskParams& p, int64_t q, int h, const Ro
         }
         __syncthreads();
         const uint32_t total = (uint32_t)sb * g.draws;
-        if (dom.rounds == 6)
+        if (dom.size <= 65536u && g.draws < 65536u) {
+            if (dom.rounds == 6)
+                walk_draws16<6>(dom, rks, bits, total, g.draws, inv_draws);
+            else
+                walk_draws16<12>(dom, rks, bits, total, g.draws, inv_draws);
+        } else {
             walk_draws<6>(dom, rks, bits, total, g.draws, inv_draws);
-        else
-            walk_draws<12>(dom, rks, bits, total, g.draws, inv_draws);
+        }
     }
     __syncthreads();
 }
@@ -301,7 +415,7 @@ __global__ __launch_bounds__(kThreads) void k_mask_count(MaskParams p, int64_t* 
     extern __shared__ __align__(16) uint32_t smem[];
     __shared__ uint32_t red[4];
     uint32_t* rks = smem;
-    uint32_t* bits = smem + kSeedBatch * kRowWords;
+    uint32_t* bits = smem + rks_words(p);
     int64_t r, q; int h;
     row_of_block(p, r, q, h);
     const RowGeom g = row_geometry(p, q);
@@ -318,7 +432,7 @@ __global__ __launch_bounds__(kThreads) void k_mask_fill(MaskParams p, const int6
     extern __shared__ __align__(16) uint32_t smem[];
     __shared__ uint32_t red[4];
     uint32_t* rks = smem;
-    uint32_t* bits = smem + kSeedBatch * kRowWords;
+    uint32_t* bits = smem + rks_words(p);
     int64_t r, q; int h;
     row_of_block(p, r, q, h);
     const int64_t base = row_ptr[r];
@@ -334,20 +448,30 @@ __global__ __launch_bounds__(kThreads) void k_mask_fill(MaskParams p, const int6
 }
 
 // ---------------------------------------------------------------------------
+// A block-uniform 64-bit value held in scalar registers.
+__device__ __forceinline__ int64_t uniform_i64(int64_t v) {
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)v);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)((uint64_t)v >> 32));
+    return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
 // One-pass build (count, scan and fill fused), used when col_idx is sized from
-// the closed-form bound.  Each workgroup takes a ticket -- rows are processed
-// in row order -- builds its row bitmap once, and finds its offset by a
-// decoupled look-back over its predecessors' status words, which live in
-// row_ptr itself (the protocol and its flags are in lookback.h).  A row
-// publishes its size before looking back (64 predecessors per step, one per
-// lane), and a ticket is only ever waited on by later tickets, whose
-// workgroups started after it; so every wait ends.  The wait is bounded
-// anyway (p.spin_limit polls): past the bound the row publishes poison and
-// writes nothing, any row whose look-back reaches a poisoned prefix does the
-// same, and k_strip_status makes the total row_ptr[R] negative, so that an
-// incomplete CSR is reported rather than used.  Status words are read and
-// written with relaxed agent-scope atomics: they carry the only data
-// exchanged.
+// the closed-form bound.  A persistent grid of workgroups takes tickets --
+// rows in row order -- and builds each row's bitmap once.  A row's offset is
+// found by a decoupled look-back over its predecessors' status words, which
+// live in row_ptr itself (the protocol and its flags are in lookback.h).  A
+// workgroup publishes a row's size as soon as its bitmap is built and keeps
+// the bitmap in LDS while it builds the next rows; it looks back for the row's
+// offset (64 predecessors per step, one per lane) and writes its keys only
+// after up to two more rows, when the predecessors, whose rows were taken
+// earlier, have almost always published their sizes.  Every wait ends: a
+// ticket is held only by a running workgroup, which publishes the row's size
+// before it waits on anything.  The wait is bounded anyway (p.spin_limit
+// polls): past the bound the row publishes poison and writes nothing, any row
+// whose look-back reaches a poisoned prefix does the same, and k_strip_status
+// makes the total row_ptr[R] negative, so that an incomplete CSR is reported
+// rather than used.  Status words are read and written with relaxed
+// agent-scope atomics: they carry the only data exchanged.
 __device__ __forceinline__ int64_t status_load(const int64_t* p) {
     return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
@@ -355,42 +479,30 @@ __device__ __forceinline__ void status_store(int64_t* p, int64_t v) {
     __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-__global__ __launch_bounds__(kThreads) void k_mask_fused(MaskParams p, int64_t* row_ptr,
-                                                         int32_t* col_idx, int64_t capacity) {
-    extern __shared__ __align__(16) uint32_t smem[];
-    __shared__ uint32_t red[4];
-    __shared__ int64_t s_ticket, s_base;
-    uint32_t* rks = smem;
-    uint32_t* bits = smem + kSeedBatch * kRowWords;
-    const int64_t R = (int64_t)p.heads * p.nq;
-    if (threadIdx.x == 0) {
-        const int64_t t = (int64_t)atomicAdd(reinterpret_cast<unsigned long long*>(row_ptr), 1ull);
-        s_ticket = t;
-        // The last ticket is the last increment of row_ptr[0]: restore it to 0.
-        if (t == R - 1) status_store(row_ptr, 0);
-    }
-    __syncthreads();
-    const int64_t r = s_ticket;
-    const int h = (int)(r / p.nq);
-    const int64_t q = p.q0 + (r - (int64_t)h * p.nq);
-    const RowGeom g = row_geometry(p, q);
-    build_row_bitmap(p, q, h, g, rks, bits);
-    const uint32_t W = (g.pool + 31u) >> 5;
-    uint32_t c = 0;
-    for (uint32_t w = threadIdx.x; w < W; w += kThreads) c += __popc(bits[w]);
-    const int64_t count = (int64_t)block_sum(c, red) + g.clique_len;
+// A row of the one-pass build whose size is published but whose keys are not
+// yet written: its bitmap waits in LDS until its offset is known.
+struct PendingRow {
+    int64_t row;
+    int64_t count;
+    RowGeom g;
+    uint32_t* bits;
+};
 
+// Find the offset of row x.row by the decoupled look-back, publish its
+// inclusive prefix and write its keys.  Block-wide; starts and ends with every
+// thread of the block present.
+__device__ void resolve_and_emit(const MaskParams& p, int64_t* row_ptr, int32_t* col_idx, int64_t capacity,
+                                 const PendingRow& x, uint32_t* red, int64_t* s_base) {
+    namespace lb = lookback;
     if (threadIdx.x < 64) {
         // Wave-wide look-back: lane i reads the status of row j-1-i, so each
         // step covers 64 predecessors.  The step ends at the nearest row whose
         // inclusive prefix is known, once every row before it is ready.
-        namespace lb = lookback;
         const int lane = threadIdx.x;
-        if (lane == 0) status_store(&row_ptr[r + 1], lb::aggregate(count));
         int64_t prefix = 0;
         bool poisoned = false;
         uint32_t spins = 0;
-        for (int64_t j = r; j > 0;) {
+        for (int64_t j = x.row; j > 0;) {
             const int64_t idx = j - lane;                       // row idx-1's status
             const int64_t v = idx > 0 ? status_load(&row_ptr[idx]) : lb::inclusive(0, false);
             const int first = lb::step_end(__ballot(lb::is_inclusive(v)), __ballot(lb::is_ready(v)));
@@ -414,17 +526,82 @@ __global__ __launch_bounds__(kThreads) void k_mask_fused(MaskParams p, int64_t* 
             j -= 64;
         }
         if (lane == 0) {
-            status_store(&row_ptr[r + 1], lb::inclusive(prefix + count, poisoned));
-            s_base = poisoned ? -1 : prefix;
+            status_store(&row_ptr[x.row + 1], lb::inclusive(prefix + x.count, poisoned));
+            *s_base = poisoned ? -1 : prefix;
         }
     }
     __syncthreads();
-    const int64_t base = s_base;
-    if (base < 0 || base > capacity) return;
-    int64_t limit = count;
-    if (limit > capacity - base) limit = capacity - base;
-    int32_t* out = col_idx + base;
-    emit_row(bits, W, out, limit, g, red);
+    const int64_t base = uniform_i64(*s_base);
+    if (base >= 0 && base <= capacity) {
+        int64_t limit = x.count;
+        if (limit > capacity - base) limit = capacity - base;
+        emit_row(x.bits, (x.g.pool + 31u) >> 5, col_idx + base, limit, x.g, red);
+    }
+}
+
+// Persistent one-pass build.  Every workgroup takes rows (tickets, in row
+// order) until none is left.  It publishes a row's size as soon as the row's
+// bitmap is built, but looks back for the row's offset only after building
+// kDepth more rows: by then its predecessors have almost always published
+// their sizes, so the look-back rarely waits.  kDepth + 1 bitmaps per
+// workgroup rotate through the rows.
+template <int kDepth>
+__global__ __launch_bounds__(kThreads, kDepth == 2 ? 6 : 8) void k_mask_fused(MaskParams p, int64_t* row_ptr,
+                                                                             int32_t* col_idx, int64_t capacity) {
+    static_assert(kDepth >= 0 && kDepth <= 2, "at most two rows wait for their offsets");
+    extern __shared__ __align__(16) uint32_t smem[];
+    __shared__ uint32_t red[4];
+    __shared__ int64_t s_ticket, s_base;
+    namespace lb = lookback;
+    uint32_t* rks = smem;
+    uint32_t* bitmaps = smem + rks_words(p);
+    const int64_t bw = bitmap_words(p);
+    const int64_t R = (int64_t)p.heads * p.nq;
+    PendingRow q0 = {}, q1 = {};
+    int n = 0;
+    for (int it = 0;; ++it) {
+        if (threadIdx.x == 0) {
+            const int64_t t = (int64_t)atomicAdd(reinterpret_cast<unsigned long long*>(row_ptr), 1ull);
+            s_ticket = t;
+            // Every workgroup takes tickets until one is past the rows, so
+            // R + gridDim.x tickets are taken in all; the last one restores
+            // row_ptr[0] to 0.
+            if (t == R + (int64_t)gridDim.x - 1) status_store(row_ptr, 0);
+        }
+        __syncthreads();   // also: the bitmap emitted last iteration is no longer read
+        const int64_t r = uniform_i64(s_ticket);
+        if (r >= R) {
+            if (kDepth > 0 && n > 0) resolve_and_emit(p, row_ptr, col_idx, capacity, q0, red, &s_base);
+            if (kDepth > 1 && n > 1) resolve_and_emit(p, row_ptr, col_idx, capacity, q1, red, &s_base);
+            break;
+        }
+        PendingRow fresh;
+        fresh.row = r;
+        fresh.bits = bitmaps + (int64_t)(it % (kDepth + 1)) * bw;
+        {
+            const int h = (int)(r / p.nq);
+            const int64_t q = p.q0 + (r - (int64_t)h * p.nq);
+            fresh.g = row_geometry(p, q);
+            build_row_bitmap(p, q, h, fresh.g, rks, fresh.bits);
+            const uint32_t W = (fresh.g.pool + 31u) >> 5;
+            uint32_t c = 0;
+            for (uint32_t w = threadIdx.x; w < W; w += kThreads) c += __popc(fresh.bits[w]);
+            fresh.count = (int64_t)__builtin_amdgcn_readfirstlane((int)block_sum(c, red)) + fresh.g.clique_len;
+            if (threadIdx.x == 0) status_store(&row_ptr[r + 1], lb::aggregate(fresh.count));
+        }
+        if (kDepth == 0) {
+            resolve_and_emit(p, row_ptr, col_idx, capacity, fresh, red, &s_base);
+            continue;
+        }
+        if (n == kDepth) {
+            resolve_and_emit(p, row_ptr, col_idx, capacity, q0, red, &s_base);
+            if (kDepth > 1) q0 = q1;
+            --n;
+        }
+        if (n == 0) q0 = fresh;
+        else q1 = fresh;
+        ++n;
+    }
 }
 
 __global__ void k_fill_i64(int64_t* x, int64_t n, int64_t v) {
@@ -502,11 +679,18 @@ __global__ __launch_bounds__(kScanThreads) void k_scan_rows(int64_t* row_ptr, in
     }
 }
 
-size_t mask_smem_bytes(const MaskParams& p) {
-    // Largest pool of the built rows: q0 + nq keys (causal) or N.
-    const int64_t span = p.causal ? p.q0 + p.nq : p.N;
-    const int64_t words = (span + 31) / 32;
-    return (size_t)(kSeedBatch * kRowWords + words) * sizeof(uint32_t);
+size_t mask_smem_bytes(const MaskParams& p, int bitmaps = 1) {
+    return (size_t)(rks_words(p) + bitmaps * bitmap_words(p)) * sizeof(uint32_t);
+}
+
+// Workgroups per CU below which a deeper one-pass pipeline costs more
+// occupancy than its shorter waits gain.
+constexpr int kMinResidentRows = 6;
+
+template <int kDepth>
+hipError_t fused_occupancy(const MaskParams& p, int* blocks) {
+    return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks, k_mask_fused<kDepth>, kThreads,
+                                                        mask_smem_bytes(p, kDepth + 1));
 }
 
 }  // namespace
@@ -528,8 +712,36 @@ hipError_t launch_mask_fused(const MaskParams& p, int64_t* row_ptr, int32_t* col
     hipLaunchKernelGGL(k_fill_i64, dim3(eb), dim3(256), 0, st, row_ptr, rows + 1, (int64_t)0);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k_mask_fused, dim3((unsigned)rows), dim3(kThreads), mask_smem_bytes(p), st, p,
-                       row_ptr, col_idx, capacity);
+    // Persistent: as many workgroups as fit on the device at once, each
+    // taking rows until none is left.
+    // Pipeline depth: the deepest (at most 2) that keeps at least 6 workgroups
+    // resident per CU; else 0 (each row looks back right after its bitmap).
+    int dev = 0, cus = 0;
+    if ((e = hipGetDevice(&dev)) != hipSuccess) return e;
+    if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess) return e;
+    int depth = 0, per_cu = 0;
+    for (int d = 2; d >= 0; --d) {
+        int b = 0;
+        e = d == 2 ? fused_occupancy<2>(p, &b) : d == 1 ? fused_occupancy<1>(p, &b) : fused_occupancy<0>(p, &b);
+        if (e != hipSuccess) return e;
+        if (b >= kMinResidentRows || d == 0) {
+            depth = d;
+            per_cu = b;
+            break;
+        }
+    }
+    int64_t grid = (int64_t)(per_cu > 0 ? per_cu : 1) * (cus > 0 ? cus : 1);
+    if (grid > rows) grid = rows;
+    const size_t smem = mask_smem_bytes(p, depth + 1);
+    if (depth == 2)
+        hipLaunchKernelGGL(k_mask_fused<2>, dim3((unsigned)grid), dim3(kThreads), smem, st, p,
+                           row_ptr, col_idx, capacity);
+    else if (depth == 1)
+        hipLaunchKernelGGL(k_mask_fused<1>, dim3((unsigned)grid), dim3(kThreads), smem, st, p,
+                           row_ptr, col_idx, capacity);
+    else
+        hipLaunchKernelGGL(k_mask_fused<0>, dim3((unsigned)grid), dim3(kThreads), smem, st, p,
+                           row_ptr, col_idx, capacity);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     const unsigned sb = (unsigned)((rows + 255) / 256);

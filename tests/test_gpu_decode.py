@@ -36,6 +36,10 @@ ROW_CASES = [
     (0, 10_000, 262144, 1, 3, 0, 0, 0, 131000, 100),
     (0, 2_000, 262144, 2, 5, 0, 0, 0, 262080, 64),
     (1, 10_000, 262144, 1, 3, 64, 1024, 4, 262100, 44),
+    # one-pass build with one row in flight per workgroup (bitmaps of 73k to
+    # 100k keys; the range below crosses 65536, so both walks run)
+    (0, 1_000, 80000, 2, 2, 0, 0, 0, 64000, 16000),
+    (1, 2_000, 100000, 1, 3, 64, 0, 0, 99000, 1000),
 ]
 
 
