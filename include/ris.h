@@ -123,7 +123,10 @@ typedef struct {
  *   phases).  The call itself still returns RIS_OK, since it does not wait
  *   for the device; check row_ptr[heads*N] >= 0 where it is read back.  The
  *   environment variable RIS_DEBUG_LOOKBACK_SPINS=<polls> lowers the bound
- *   (a test hook: 0 gives up at the first wait).
+ *   (a test hook: 0 gives up at the first wait), and RIS_DEBUG_POISON_ROW=<r>
+ *   makes row r (of the rows built, head-major) give up without waiting (a
+ *   test hook: row r, any row whose look-back reaches its status, and the
+ *   total are then reported as -1).
  * Fill phase (col_idx != NULL, smaller capacity): row_ptr must hold the
  *   count phase's output for the same descriptor; the call first reads
  *   row_ptr[heads*N] (synchronising the stream), returns RIS_E_CAPACITY,

@@ -356,9 +356,10 @@ __device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* r
 // Write the row: the set bits of bits[0, W) as keys 32 w + b, ascending, at
 // out[0, ..), then the Structural clique; nothing at out[limit] or beyond.
 // A lane's keys of one word are contiguous in out, so it writes them four at
-// a time with 16-byte stores once its position is 16-byte aligned (scalar
-// stores at the two ends): a quarter of the store instructions of one key
-// per store.
+// a time with 16-byte stores (global stores need only 4-byte alignment) and
+// the last one to three with an 8- and a 4-byte store: the store
+// instructions, whose address processing limits this loop, are about a
+// quarter of one key per store.
 __device__ void emit_row(const uint32_t* bits, uint32_t W, int32_t* out, int64_t limit, const RowGeom& g,
                          uint32_t* red) {
     uint32_t done = 0;
@@ -373,11 +374,8 @@ __device__ void emit_row(const uint32_t* bits, uint32_t W, int32_t* out, int64_t
             word &= word - 1u;
             return k0 + (int32_t)b;
         };
-        while (word && (reinterpret_cast<uintptr_t>(out + pos) & 15u)) {
-            const int32_t k = next_key();
-            if (pos < limit) out[pos] = k;
-            ++pos;
-        }
+        // Groups of four keys as 16-byte stores at any 4-byte-aligned position,
+        // then the last one to three keys.
         while (__popc(word) >= 4) {
             const int32_t a = next_key(), b = next_key(), c = next_key(), d = next_key();
             if (pos + 4 <= limit) {
@@ -389,7 +387,16 @@ __device__ void emit_row(const uint32_t* bits, uint32_t W, int32_t* out, int64_t
             }
             pos += 4;
         }
-        while (word) {
+        if (__popc(word) >= 2) {
+            const int32_t a = next_key(), b = next_key();
+            if (pos + 2 <= limit) {
+                *reinterpret_cast<int2*>(out + pos) = make_int2(a, b);
+            } else if (pos < limit) {
+                out[pos] = a;
+            }
+            pos += 2;
+        }
+        if (word) {
             const int32_t k = next_key();
             if (pos < limit) out[pos] = k;
             ++pos;
@@ -500,9 +507,9 @@ __device__ void resolve_and_emit(const MaskParams& p, int64_t* row_ptr, int32_t*
         // inclusive prefix is known, once every row before it is ready.
         const int lane = threadIdx.x;
         int64_t prefix = 0;
-        bool poisoned = false;
+        bool poisoned = x.row == p.poison_row;   // test hook: as if the wait had given up
         uint32_t spins = 0;
-        for (int64_t j = x.row; j > 0;) {
+        for (int64_t j = poisoned ? 0 : x.row; j > 0;) {
             const int64_t idx = j - lane;                       // row idx-1's status
             const int64_t v = idx > 0 ? status_load(&row_ptr[idx]) : lb::inclusive(0, false);
             const int first = lb::step_end(__ballot(lb::is_inclusive(v)), __ballot(lb::is_ready(v)));

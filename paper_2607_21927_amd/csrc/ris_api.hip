@@ -63,9 +63,23 @@ uint32_t lookback_spin_limit() {
     return 1u << 24;
 }
 
+// RIS_DEBUG_POISON_ROW=<r>: a second test hook.  Row r of the one-pass
+// build publishes poison in place of its look-back, as if its wait had given
+// up, so that the poison path runs whatever the timing (-1 = none).
+int64_t lookback_poison_row() {
+    const char* s = getenv("RIS_DEBUG_POISON_ROW");
+    if (s && *s) {
+        char* end = nullptr;
+        const long long v = strtoll(s, &end, 10);
+        if (end && *end == '\0' && v >= 0) return (int64_t)v;
+    }
+    return -1;
+}
+
 MaskParams make_params(const ris_mask_desc* d, int64_t q0, int64_t nq) {
     MaskParams p;
     p.spin_limit = lookback_spin_limit();
+    p.poison_row = lookback_poison_row();
     p.q0 = q0;
     p.nq = nq;
     p.seed = d->seed;

@@ -22,6 +22,7 @@ struct MaskParams {
     int64_t q0;       // rows [q0, q0 + nq) of each head are built;
     int64_t nq;       // row r = h * nq + (q - q0)
     uint32_t spin_limit;   // one-pass build: look-back polls before a row gives up
+    int64_t poison_row;    // one-pass build test hook: this row publishes poison (-1 = none)
 };
 
 hipError_t launch_mask_count(const MaskParams& p, int64_t* row_ptr, hipStream_t st);

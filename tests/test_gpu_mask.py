@@ -180,18 +180,13 @@ def test_union_size_matches_its_expectation(name):
     assert abs(nnz - mean) < 5 * sd, (nnz, mean, sd)
 
 
-def test_lookback_give_up_is_reported(monkeypatch):
-    """The one-pass build's bounded wait, forced to give up from the host
-    (RIS_DEBUG_LOOKBACK_SPINS=0: a row that finds a predecessor not ready
-    gives up at once, so every kernel exits normally).  A row that gives up,
-    or whose look-back meets a poisoned prefix, writes no keys and -1 as its
-    entry; the total row_ptr[R] is then -1 and the binding's check raises.
-    Nothing is written past col_idx's capacity, and every row that was not
-    poisoned still holds exactly the oracle's keys at its offset.  A build
+def _give_up_case(ris, monkeypatch, env, value, must_poison):
+    """Build with a give-up forced from the host (env=value), then check the
+    reported result: nothing written past col_idx's capacity; if any row is
+    poisoned, the total is -1, the binding's check raises, and every row that
+    was not poisoned holds exactly the oracle's keys at its offset.  A build
     with the normal bound afterwards is exact."""
-    ris = need_gpu()
     sp = spec_of(0, 10_000, 16384, 2, 3)
-    say("look-back give-up: N=16384 heads=2 S=3, spin limit 0")
     want_rp, want_ci = o_geo.build_csr(sp)
     d = desc_of(ris, sp)
     cap = ris.mask_nnz_bound(d)
@@ -199,15 +194,17 @@ def test_lookback_give_up_is_reported(monkeypatch):
     R = sp.heads * sp.N
     rp = torch.empty(R + 1, dtype=torch.int64, device="cuda")
     ci = torch.full((cap + guard,), -7, dtype=torch.int32, device="cuda")
-    monkeypatch.setenv("RIS_DEBUG_LOOKBACK_SPINS", "0")
+    monkeypatch.setenv(env, str(value))
     ris.mask_build(d, rp, ci, col_capacity=cap)
     torch.cuda.synchronize()
-    monkeypatch.delenv("RIS_DEBUG_LOOKBACK_SPINS")
+    monkeypatch.delenv(env)
     rp_h, ci_h = rp.cpu().numpy(), ci.cpu().numpy()
     assert (ci_h[cap:] == -7).all(), "write past the capacity"
     counts = np.diff(want_rp)
     poisoned = np.flatnonzero(rp_h[1:] < 0)
     say(f"  total {rp_h[-1]}, {len(poisoned)} of {R} rows poisoned")
+    if must_poison:
+        assert rp_h[-1] == -1 and len(poisoned) > 0
     if rp_h[-1] >= 0:
         # no row had to wait: the build is complete and exact
         assert len(poisoned) == 0
@@ -227,3 +224,27 @@ def test_lookback_give_up_is_reported(monkeypatch):
     rp2, ci2 = gpu_csr(ris, sp, use_bound=True)
     assert np.array_equal(rp2.cpu().numpy(), want_rp)
     assert np.array_equal(ci2.cpu().numpy()[: want_rp[-1]], want_ci)
+    return rp_h, poisoned
+
+
+def test_lookback_give_up_is_reported(monkeypatch):
+    """The one-pass build's bounded wait, forced to give up from the host
+    (RIS_DEBUG_LOOKBACK_SPINS=0: a row that finds a predecessor not ready
+    gives up at once, so every kernel exits normally).  Whether any row has
+    to wait depends on the timing; the reported result must be right either
+    way."""
+    ris = need_gpu()
+    say("look-back give-up: N=16384 heads=2 S=3, spin limit 0")
+    _give_up_case(ris, monkeypatch, "RIS_DEBUG_LOOKBACK_SPINS", 0, must_poison=False)
+
+
+def test_forced_poison_row_is_reported(monkeypatch):
+    """The poison path whatever the timing: RIS_DEBUG_POISON_ROW makes one
+    row publish poison in place of its look-back.  That row and the total
+    must read -1, and the rest must be as above."""
+    ris = need_gpu()
+    r = 2 * 16384 // 3
+    say(f"forced poison: N=16384 heads=2 S=3, row {r}")
+    rp_h, poisoned = _give_up_case(ris, monkeypatch, "RIS_DEBUG_POISON_ROW", r, must_poison=True)
+    assert rp_h[r + 1] == -1 and r in poisoned
+    assert (rp_h[1:r + 1] >= 0).all(), "a row before the poisoned one was poisoned"
