@@ -361,45 +361,64 @@ __device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* r
 // instructions, whose address processing limits this loop, are about a
 // quarter of one key per store.
 __device__ void emit_row(const uint32_t* bits, uint32_t W, int32_t* out, int64_t limit, const RowGeom& g,
-                         uint32_t* red) {
+                         uint32_t* red, int64_t count) {
+    // The whole row fits below limit in every valid build; the guarded path
+    // is for a truncated or inconsistent row_ptr.
+    const bool whole = limit >= count;
     uint32_t done = 0;
     for (uint32_t w0 = 0; w0 < W; w0 += kThreads) {
         const uint32_t w = w0 + threadIdx.x;
         uint32_t word = w < W ? bits[w] : 0u;
         uint32_t total;
-        int64_t pos = done + block_exclusive_scan(__popc(word), red, &total);
+        const uint32_t pos0 = done + block_exclusive_scan(__popc(word), red, &total);
         const int32_t k0 = (int32_t)(w * 32u);
         auto next_key = [&]() {
-            const uint32_t b = __ffs(word) - 1u;
+            const uint32_t b = (uint32_t)__builtin_ctz(word);   // v_ffbl_b32 (word != 0 here)
             word &= word - 1u;
             return k0 + (int32_t)b;
         };
         // Groups of four keys as 16-byte stores at any 4-byte-aligned position,
         // then the last one to three keys.
-        while (__popc(word) >= 4) {
-            const int32_t a = next_key(), b = next_key(), c = next_key(), d = next_key();
-            if (pos + 4 <= limit) {
-                *reinterpret_cast<int4*>(out + pos) = make_int4(a, b, c, d);
-            } else {
-                if (pos < limit) out[pos] = a;
-                if (pos + 1 < limit) out[pos + 1] = b;
-                if (pos + 2 < limit) out[pos + 2] = c;
+        if (whole) {
+            int32_t* o = out + pos0;
+            for (uint32_t n = __popc(word); n >= 4u; n -= 4u) {
+                const int32_t a = next_key(), b = next_key(), c = next_key(), d = next_key();
+                *reinterpret_cast<int4*>(o) = make_int4(a, b, c, d);
+                o += 4;
             }
-            pos += 4;
-        }
-        if (__popc(word) >= 2) {
-            const int32_t a = next_key(), b = next_key();
-            if (pos + 2 <= limit) {
-                *reinterpret_cast<int2*>(out + pos) = make_int2(a, b);
-            } else if (pos < limit) {
-                out[pos] = a;
+            if (__popc(word) >= 2) {
+                const int32_t a = next_key(), b = next_key();
+                *reinterpret_cast<int2*>(o) = make_int2(a, b);
+                o += 2;
             }
-            pos += 2;
-        }
-        if (word) {
-            const int32_t k = next_key();
-            if (pos < limit) out[pos] = k;
-            ++pos;
+            if (word) *o = next_key();
+        } else {
+            int64_t pos = pos0;
+            while (__popc(word) >= 4) {
+                const int32_t a = next_key(), b = next_key(), c = next_key(), d = next_key();
+                if (pos + 4 <= limit) {
+                    *reinterpret_cast<int4*>(out + pos) = make_int4(a, b, c, d);
+                } else {
+                    if (pos < limit) out[pos] = a;
+                    if (pos + 1 < limit) out[pos + 1] = b;
+                    if (pos + 2 < limit) out[pos + 2] = c;
+                }
+                pos += 4;
+            }
+            if (__popc(word) >= 2) {
+                const int32_t a = next_key(), b = next_key();
+                if (pos + 2 <= limit) {
+                    *reinterpret_cast<int2*>(out + pos) = make_int2(a, b);
+                } else if (pos < limit) {
+                    out[pos] = a;
+                }
+                pos += 2;
+            }
+            if (word) {
+                const int32_t k = next_key();
+                if (pos < limit) out[pos] = k;
+                ++pos;
+            }
         }
         done += total;
     }
@@ -450,8 +469,10 @@ __global__ __launch_bounds__(kThreads) void k_mask_fill(MaskParams p, const int6
     const RowGeom g = row_geometry(p, q);
     build_row_bitmap(p, q, h, g, rks, bits);
     const uint32_t W = (g.pool + 31u) >> 5;
-    int32_t* out = col_idx + base;
-    emit_row(bits, W, out, limit, g, red);
+    uint32_t c = 0;
+    for (uint32_t w = threadIdx.x; w < W; w += kThreads) c += __popc(bits[w]);
+    const int64_t count = (int64_t)block_sum(c, red) + g.clique_len;
+    emit_row(bits, W, col_idx + base, limit, g, red, count);
 }
 
 // ---------------------------------------------------------------------------
@@ -542,7 +563,7 @@ __device__ void resolve_and_emit(const MaskParams& p, int64_t* row_ptr, int32_t*
     if (base >= 0 && base <= capacity) {
         int64_t limit = x.count;
         if (limit > capacity - base) limit = capacity - base;
-        emit_row(x.bits, (x.g.pool + 31u) >> 5, col_idx + base, limit, x.g, red);
+        emit_row(x.bits, (x.g.pool + 31u) >> 5, col_idx + base, limit, x.g, red, x.count);
     }
 }
 
