@@ -1,8 +1,9 @@
 // Geometry kernels: per-row key sets of the seed ensemble, emitted as CSR.
 //
-// One workgroup builds one row (kv_head, q).  The row's pool is a bitmap in
-// LDS; every (seed, draw) pair of the ensemble is spread over the 256 lanes,
-// each lane evaluates the keyed permutation and ORs its key into the bitmap.
+// Each row (kv_head, q) is built by one workgroup.  The row's pool is a
+// bitmap in LDS; every (seed, draw) pair of the ensemble is spread over the
+// 256 lanes, each lane evaluates the keyed permutation and ORs its key into
+// the bitmap.
 // The bitmap *is* the union over seeds (the paper merges every seed into one
 // master set and discards the seed; Methods, "Memory-Bounded Geometry
 // Generation"), and reading it in word order yields the row ascending and
@@ -571,8 +572,8 @@ __device__ void resolve_and_emit(const MaskParams& p, int64_t* row_ptr, int32_t*
 // order) until none is left.  It publishes a row's size as soon as the row's
 // bitmap is built, but looks back for the row's offset only after building
 // kDepth more rows: by then its predecessors have almost always published
-// their sizes, so the look-back rarely waits.  kDepth + 1 bitmaps per
-// workgroup rotate through the rows.
+// their sizes, so the look-back rarely waits (kDepth = 0: at once).
+// kDepth + 1 bitmaps per workgroup rotate through the rows.
 template <int kDepth>
 __global__ __launch_bounds__(kThreads, kDepth == 2 ? 6 : 8) void k_mask_fused(MaskParams p, int64_t* row_ptr,
                                                                              int32_t* col_idx, int64_t capacity) {
