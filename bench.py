@@ -348,8 +348,8 @@ def measured_traffic(record, kernel_source):
     """Bytes per launch past the L2 caches (FETCH_SIZE + WRITE_SIZE, each
     scaled by its reading for a device copy of known size) from the committed
     rocprofv3 counter record profiles/<record>_traffic.txt, or None when no
-    record exists or the kernel source changed since the counters were
-    taken."""
+    record exists or the kernel source or the device headers it includes
+    changed since the counters were taken."""
     import hashlib
     path = os.path.join(PROFILES, f"{record}_traffic.txt")
     if not os.path.exists(path):
@@ -360,6 +360,19 @@ def measured_traffic(record, kernel_source):
     if not os.path.exists(src) or rec.get("source") != kernel_source:
         return None
     if hashlib.sha256(open(src, "rb").read()).hexdigest() != rec.get("source_sha256"):
+        return None
+    # the device headers the kernel includes (inline helpers such as the
+    # dispatch decision live there), hashed one after the other
+    heads = [h for h in rec.get("headers", "").split(",") if h]
+    if not heads:
+        return None
+    hh = hashlib.sha256()
+    for h in heads:
+        hp = os.path.join(ROOT, h)
+        if not os.path.exists(hp):
+            return None
+        hh.update(open(hp, "rb").read())
+    if hh.hexdigest() != rec.get("headers_sha256"):
         return None
     return float(rec["traffic_bytes"])
 

@@ -233,8 +233,10 @@ typedef struct {
     int32_t causal;          /* as in ris_mask_desc                             */
     int32_t algo;            /* ris_attn_algo: GATHER = per-row gather kernel;  */
                              /* TILE = 32-row tiles on MFMA (bf16 only); AUTO  */
-                             /* = per 32-row tile, TILE when the tile's union  */
-                             /* density is >= 6.8%, GATHER otherwise           */
+                             /* = per 32-row tile, TILE when the tile's entries */
+                             /* fill >= 5% of rows x keys over the key range   */
+                             /* its rows touch (first to last key, at most the */
+                             /* causal span), GATHER otherwise                 */
 } ris_attn_desc;
 
 /*

@@ -124,9 +124,16 @@ int64_t nnz_bound(const MaskParams& p) {
 
 int hip_status(hipError_t e) { return e == hipSuccess ? RIS_OK : RIS_E_HIP; }
 
-// Union density of a 32-row tile above which the tiled kernel is faster than
-// the gather kernel (measured crossover on MI355X, the same at N = 16k..64k).
-constexpr float kAutoDensity = 0.068f;
+// Union density of a 32-row tile (entries over rows x the key range the
+// tiled kernel walks) from which the tiled kernel takes it.  Measured on
+// MI355X for layers whose tiles are all alike (Qwen2 shape, Stochastic 1%,
+// 4-6 seeds, N = 32k and 64k), the two kernels cross near 5.7%; the gather
+// kernel left with only a minority of a layer's tiles runs below its
+// full-load rate, which moves the best split for mixed layers lower (32k
+// Structural with B = 64: 4.5 ms at 6.8%, 3.8 ms at 5%), so the threshold
+// sits at 5%, still above the 4.9% union of five seeds, which the gather
+// kernel serves 15% faster.
+constexpr float kAutoDensity = 0.05f;
 
 }  // namespace
 
@@ -277,7 +284,8 @@ int ris_sparse_attn(const void* Q, const void* K, const void* V, const int64_t* 
         return hip_status(ris::launch_attn_tile(a, s));
     }
     // AUTO: per 32-row tile by union density.  The tiled kernel's cost grows
-    // with the key span, the gather kernel's with the entries (kAutoDensity).
+    // with the key range its rows touch, the gather kernel's with the entries
+    // (kAutoDensity).
     a.tau = kAutoDensity;
     const int st = hip_status(ris::launch_attn_tile(a, s));
     if (st != RIS_OK) return st;

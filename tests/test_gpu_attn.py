@@ -142,24 +142,72 @@ def test_tile_kernel_paper_block_rule_and_sparse_rows():
 
 
 def test_auto_dispatch_mixed_density():
-    """AUTO splits by 32-row tile: at 1% x 6 seeds the first tiles (k >= 1 on
-    a short prefix) are dense and go to the tiled kernel, later tiles (~5.9%
+    """AUTO splits by 32-row tile: at 1% x 4 seeds the first tiles (k >= 1 on
+    a short prefix) are dense and go to the tiled kernel, later tiles (~3.9%
     union) to the gather kernel; the result is the oracle's either way, and
-    each tile's rows equal the output of the kernel its density selects."""
+    each tile's rows equal the output of the kernel the library's rule
+    selects (entries >= 5% of rows x keys over the causal span or, failing
+    that, over the range from the rows' first to their last key)."""
     from oracle import geometry as o_geo
-    N, ppm, S = 2500, 10_000, 6
+    N, ppm, S = 2500, 10_000, 4
     got, want, _ = run_case(12, 2, N, 128, 0, ppm, S, algo=0)
     assert float(np.abs(got - want).max()) <= tight_tol(0, 5.5)
     got_g, _, _ = run_case(12, 2, N, 128, 0, ppm, S, algo=1)
     got_t, _, _ = run_case(12, 2, N, 128, 0, ppm, S, algo=2)
-    tau = float(np.float32(0.068))           # the library's threshold, as float32
-    sp = spec_of(0, ppm, N, 2, S)
+    dense = auto_dense_rows(spec_of(0, ppm, N, 2, S), 0, N, causal=True)
+    assert dense.any() and (~dense).any()
+    assert np.array_equal(got[:6][:, ~dense], got_g[:6][:, ~dense])
+    assert np.array_equal(got[:6][:, dense], got_t[:6][:, dense])
+
+
+def auto_dense_rows(sp, g, N, causal):
+    """Rows of KV head g whose 32-row tile AUTO gives to the tiled kernel, by
+    the library's rule restated: threshold 5% (as float32), entries against
+    rows x causal span first, then against rows x the key range from the
+    rows' smallest first key to their largest last key (clamped to [0, N),
+    at most the span)."""
+    from oracle import geometry as o_geo
+    tau = float(np.float32(0.05))
     dense = np.zeros(N, dtype=bool)
     for q0 in range(0, N, 32):
         q1 = min(N, q0 + 32)
+        sets = o_geo.row_sets(sp, g, np.arange(q0, q1))
+        nnz = sum(len(x) for x in sets)
+        rows = q1 - q0
+        span = q1 if causal else N
+        if nnz >= tau * rows * span:
+            dense[q0:q1] = True
+            continue
+        firsts = [max(int(x[0]), 0) for x in sets if len(x)]
+        lasts = [min(int(x[-1]), N - 1) for x in sets if len(x)]
+        pairs = [(f, l) for f, l in zip(firsts, lasts) if f <= l]
+        rng = max(l for _, l in pairs) - min(f for f, _ in pairs) + 1 if pairs else 1
+        dense[q0:q1] = nnz >= tau * rows * min(rng, span)
+    return dense
+
+
+def test_auto_dispatch_structural_clique_tiles():
+    """Structural tiles whose rows hold only their local clique (k(q) below
+    the clique) touch one or two key blocks: sparse over the causal span, so
+    AUTO gives them to the tiled kernel only by the key range their rows
+    touch.  Tiles with long-range draws spread over the span stay with the
+    gather kernel.  Rows equal the selected kernel's output and the oracle's."""
+    from oracle import geometry as o_geo
+    N, ppm, S, B = 3000, 10_000, 3, 64
+    got, want, _ = run_case(12, 2, N, 128, 1, ppm, S, algo=0, block=B)
+    assert float(np.abs(got - want).max()) <= tight_tol(0, 5.5)
+    got_g, _, _ = run_case(12, 2, N, 128, 1, ppm, S, algo=1, block=B)
+    got_t, _, _ = run_case(12, 2, N, 128, 1, ppm, S, algo=2, block=B)
+    sp = spec_of(1, ppm, N, 2, S, block=B)
+    dense = auto_dense_rows(sp, 0, N, causal=True)
+    by_span = np.zeros(N, dtype=bool)
+    tau = float(np.float32(0.05))
+    for q0 in range(0, N, 32):
+        q1 = min(N, q0 + 32)
         nnz = sum(len(x) for x in o_geo.row_sets(sp, 0, np.arange(q0, q1)))
-        dense[q0:q1] = nnz >= tau * (q1 - q0) * q1
-    assert dense.any() and (~dense).any()
+        by_span[q0:q1] = nnz >= tau * (q1 - q0) * q1
+    assert (dense & ~by_span).any()      # tiles the key range moves to the tiled kernel
+    assert (~dense).any()                # and tiles left with the gather kernel
     assert np.array_equal(got[:6][:, ~dense], got_g[:6][:, ~dense])
     assert np.array_equal(got[:6][:, dense], got_t[:6][:, dense])
 
