@@ -234,9 +234,9 @@ typedef struct {
     int32_t algo;            /* ris_attn_algo: GATHER = per-row gather kernel;  */
                              /* TILE = 32-row tiles on MFMA (bf16 only); AUTO  */
                              /* = per 32-row tile, TILE when the tile's entries */
-                             /* fill >= 5% of rows x keys over the key range   */
-                             /* its rows touch (first to last key, at most the */
-                             /* causal span), GATHER otherwise                 */
+                             /* fill >= 5% of rows x keys over the causal span */
+                             /* or over the range from its first CSR entry to  */
+                             /* its last, GATHER otherwise                     */
 } ris_attn_desc;
 
 /*

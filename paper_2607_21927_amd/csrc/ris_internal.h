@@ -60,38 +60,28 @@ struct AttnParams {
 // Rows per tile of the tiled kernel; also the unit of the dispatch decision.
 constexpr int kTileRows = 32;
 
-// Density decision for the tile of rows [q0, q0 + kTileRows) of KV head g,
-// taken by a whole wave (every lane active, uniform arguments; the result is
-// the same in every lane and in every wave that asks).  The tiled kernel's
-// cost follows the key range it walks, the gather kernel's the entries, so a
-// tile is dense when its entries fill at least a fraction tau of rows x keys
-// over the range from its rows' smallest first key to their largest last
-// key, capped at the key span [0, q1) (causal) or [0, N).  Tiles dense over
-// the whole span are settled by two reads of row_ptr; the others read every
-// row's first and last key.
+// Density decision for the tile of rows [q0, q0 + kTileRows) of KV head g.
+// The tiled kernel's cost follows the key range it walks, the gather
+// kernel's the entries, so a tile is dense when its entries fill at least a
+// fraction tau of rows x keys over the causal span [0, q1) (or [0, N)) or,
+// failing that, over the range from the tile's first CSR entry (the first
+// key of its first non-empty row) to its last (the last key of its last
+// non-empty row), capped at the span.  Two reads of row_ptr, and two of
+// col_idx for tiles sparse over the span; every thread that asks gets the
+// same answer.
 __device__ __forceinline__ bool tile_is_dense(const AttnParams& a, int g, int64_t q0) {
     const int64_t q1 = q0 + kTileRows < a.N ? q0 + kTileRows : a.N;
     const int64_t* rp = a.row_ptr + (int64_t)g * a.N;
-    const int64_t nnz = rp[q1] - rp[q0];
+    const int64_t s0 = rp[q0], s1 = rp[q1];
+    const int64_t nnz = s1 - s0;
     const double rows = (double)(q1 - q0);
     const int64_t span = a.causal ? q1 : a.N;
     if ((double)nnz >= (double)a.tau * rows * (double)span) return true;
-    const int lane = threadIdx.x & 63;
-    int lo = 0x7FFFFFFF, hi = -1;
-    if (lane < q1 - q0) {
-        const int64_t s = rp[q0 + lane], e = rp[q0 + lane + 1];
-        if (s >= 0 && e > s) {
-            int f = a.col_idx[s], l = a.col_idx[e - 1];
-            if (f < 0) f = 0;
-            if ((int64_t)l > a.N - 1) l = (int)(a.N - 1);
-            if (f <= l) { lo = f; hi = l; }
-        }
-    }
-    for (int off = 32; off > 0; off >>= 1) {
-        lo = min(lo, __shfl_xor(lo, off));
-        hi = max(hi, __shfl_xor(hi, off));
-    }
-    int64_t range = hi >= lo ? (int64_t)hi - lo + 1 : 1;
+    if (s0 < 0 || nnz <= 0) return false;
+    int64_t f = a.col_idx[s0], l = a.col_idx[s1 - 1];
+    if (f < 0) f = 0;
+    if (l > a.N - 1) l = a.N - 1;
+    int64_t range = l >= f ? l - f + 1 : 1;
     if (range > span) range = span;
     return (double)nnz >= (double)a.tau * rows * (double)range;
 }

@@ -147,7 +147,7 @@ def test_auto_dispatch_mixed_density():
     union) to the gather kernel; the result is the oracle's either way, and
     each tile's rows equal the output of the kernel the library's rule
     selects (entries >= 5% of rows x keys over the causal span or, failing
-    that, over the range from the rows' first to their last key)."""
+    that, over the range from the tile's first CSR entry to its last)."""
     from oracle import geometry as o_geo
     N, ppm, S = 2500, 10_000, 4
     got, want, _ = run_case(12, 2, N, 128, 0, ppm, S, algo=0)
@@ -164,25 +164,23 @@ def auto_dense_rows(sp, g, N, causal):
     """Rows of KV head g whose 32-row tile AUTO gives to the tiled kernel, by
     the library's rule restated: threshold 5% (as float32), entries against
     rows x causal span first, then against rows x the key range from the
-    rows' smallest first key to their largest last key (clamped to [0, N),
-    at most the span)."""
+    tile's first CSR entry to its last (clamped to [0, N), at most the
+    span)."""
     from oracle import geometry as o_geo
     tau = float(np.float32(0.05))
     dense = np.zeros(N, dtype=bool)
     for q0 in range(0, N, 32):
         q1 = min(N, q0 + 32)
-        sets = o_geo.row_sets(sp, g, np.arange(q0, q1))
-        nnz = sum(len(x) for x in sets)
+        keys = np.concatenate(o_geo.row_sets(sp, g, np.arange(q0, q1)))
+        nnz = len(keys)
         rows = q1 - q0
         span = q1 if causal else N
         if nnz >= tau * rows * span:
             dense[q0:q1] = True
-            continue
-        firsts = [max(int(x[0]), 0) for x in sets if len(x)]
-        lasts = [min(int(x[-1]), N - 1) for x in sets if len(x)]
-        pairs = [(f, l) for f, l in zip(firsts, lasts) if f <= l]
-        rng = max(l for _, l in pairs) - min(f for f, _ in pairs) + 1 if pairs else 1
-        dense[q0:q1] = nnz >= tau * rows * min(rng, span)
+        elif nnz > 0:
+            f, l = max(int(keys[0]), 0), min(int(keys[-1]), N - 1)
+            rng = l - f + 1 if l >= f else 1
+            dense[q0:q1] = nnz >= tau * rows * min(rng, span)
     return dense
 
 
