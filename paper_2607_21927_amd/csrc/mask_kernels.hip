@@ -196,6 +196,17 @@ __device__ __forceinline__ void walk_draws(const FeistelDomain& dom, const uint3
 // that crosses it moves into the other walker's seed and copies that walker's
 // round keys from the other half of KM and KX.  The set of draws and each
 // draw's walk are those of walk_draws, so the bitmap is identical.
+// One step of the lane's count of draws not yet started (never negative):
+// true when none was left, else the count drops by one.  A single clamped
+// subtract does both: its borrow is the branch's lane mask, and the clamp
+// keeps an exhausted count at 0, so the other walker stops at its next draw
+// too.
+__device__ __forceinline__ bool take_last(int& rem) {
+    uint64_t borrow;
+    asm volatile("v_sub_co_u32 %0, %1, %2, 1 clamp" : "=v"(rem), "=s"(borrow) : "v"(rem));
+    return __builtin_amdgcn_inverse_ballot_w64(borrow);
+}
+
 template <int ROUNDS>
 __device__ __forceinline__ void walk_draws16(const FeistelDomain& dom, const uint32_t* rks,
                                              uint32_t* bits, uint32_t total, uint32_t draws,
@@ -237,7 +248,7 @@ __device__ __forceinline__ void walk_draws16(const FeistelDomain& dom, const uin
             uint32_t w = __builtin_amdgcn_ubfe(X, 5, 11);
             asm("" : "+v"(w));
             atomicOr(&bits[w], 1u << (X & 31u));
-            if (--rem < 0) {
+            if (take_last(rem)) {
                 actA = false;
             } else {
                 ++J;
@@ -256,7 +267,7 @@ __device__ __forceinline__ void walk_draws16(const FeistelDomain& dom, const uin
             uint32_t w = X >> 21;
             asm("" : "+v"(w));
             atomicOr(&bits[w], 1u << ((X >> 16) & 31u));
-            if (--rem < 0) {
+            if (take_last(rem)) {
                 actB = false;
             } else {
                 if (J < 0x10000u) {
