@@ -207,6 +207,15 @@ __device__ __forceinline__ bool take_last(int& rem) {
     return __builtin_amdgcn_inverse_ballot_w64(borrow);
 }
 
+// Walker B's step to the previous draw: the high half of J (B's draw
+// index) drops by one; true when it was 0, which the subtract's borrow
+// reports as the branch's lane mask (the half then reads 0xFFFF).
+__device__ __forceinline__ bool step_down_wraps(uint32_t& J) {
+    uint64_t borrow;
+    asm volatile("v_sub_co_u32 %0, %1, %2, %3" : "=v"(J), "=s"(borrow) : "v"(J), "s"(0x10000u));
+    return __builtin_amdgcn_inverse_ballot_w64(borrow);
+}
+
 template <int ROUNDS>
 __device__ __forceinline__ void walk_draws16(const FeistelDomain& dom, const uint32_t* rks,
                                              uint32_t* bits, uint32_t total, uint32_t draws,
@@ -270,15 +279,16 @@ __device__ __forceinline__ void walk_draws16(const FeistelDomain& dom, const uin
             if (take_last(rem)) {
                 actB = false;
             } else {
-                if (J < 0x10000u) {
-                    J |= draws << 16;
+                if (step_down_wraps(J)) {
+                    // B's draw index was 0 and its half now reads 0xFFFF:
+                    // it continues at draws - 1 of the previous seed
+                    J -= (0x10000u - draws) << 16;
 #pragma unroll
                     for (int r = 0; r < ROUNDS; ++r) {
                         KM[r] = __builtin_amdgcn_perm(KM[r], KM[r], 0x01000100u);
                         KX[r] = __builtin_amdgcn_perm(KX[r], KX[r], 0x01000100u);
                     }
                 }
-                J -= 0x10000u;
                 X = __builtin_amdgcn_perm(J, X, 0x07060100u);
             }
         }
