@@ -507,7 +507,8 @@ __device__ __forceinline__ int64_t uniform_i64(int64_t v) {
 
 // One-pass build (count, scan and fill fused), used when col_idx is sized from
 // the closed-form bound.  A persistent grid of workgroups takes tickets --
-// rows in row order -- and builds each row's bitmap once.  A row's offset is
+// one or two consecutive rows each, in row order -- and builds each row's
+// bitmap once.  A row's offset is
 // found by a decoupled look-back over its predecessors' status words, which
 // live in row_ptr itself (the protocol and its flags are in lookback.h).  A
 // workgroup publishes a row's size as soon as its bitmap is built and keeps
@@ -515,8 +516,10 @@ __device__ __forceinline__ int64_t uniform_i64(int64_t v) {
 // offset (64 predecessors per step, one per lane) and writes its keys only
 // after up to two more rows, when the predecessors, whose rows were taken
 // earlier, have almost always published their sizes.  Every wait ends: a
-// ticket is held only by a running workgroup, which publishes the row's size
-// before it waits on anything.  The wait is bounded anyway (p.spin_limit
+// row is held only by a running workgroup, and a workgroup waits only for
+// rows below the one it resolves, each of which its holder builds and
+// publishes after waits for still smaller rows (induction over the rows).
+// The wait is bounded anyway (p.spin_limit
 // polls): past the bound the row publishes poison and writes nothing, any row
 // whose look-back reaches a poisoned prefix does the same, and k_strip_status
 // makes the total row_ptr[R] negative, so that an incomplete CSR is reported
@@ -589,13 +592,14 @@ __device__ void resolve_and_emit(const MaskParams& p, int64_t* row_ptr, int32_t*
     }
 }
 
-// Persistent one-pass build.  Every workgroup takes rows (tickets, in row
-// order) until none is left.  It publishes a row's size as soon as the row's
+// Persistent one-pass build.  Every workgroup takes rows (tickets of
+// kRowsPerTicket consecutive rows, in row order) until none is left.  It
+// publishes a row's size as soon as the row's
 // bitmap is built, but looks back for the row's offset only after building
 // kDepth more rows: by then its predecessors have almost always published
 // their sizes, so the look-back rarely waits (kDepth = 0: at once).
 // kDepth + 1 bitmaps per workgroup rotate through the rows.
-template <int kDepth>
+template <int kDepth, int kRowsPerTicket>
 __global__ __launch_bounds__(kThreads, kDepth == 2 ? 6 : 8) void k_mask_fused(MaskParams p, int64_t* row_ptr,
                                                                              int32_t* col_idx, int64_t capacity) {
     static_assert(kDepth >= 0 && kDepth <= 2, "at most two rows wait for their offsets");
@@ -609,14 +613,31 @@ __global__ __launch_bounds__(kThreads, kDepth == 2 ? 6 : 8) void k_mask_fused(Ma
     const int64_t R = (int64_t)p.heads * p.nq;
     PendingRow q0 = {}, q1 = {};
     int n = 0;
+    // Tickets that carry rows; every workgroup takes tickets until one is
+    // past them, so T + gridDim.x tickets are taken in all, and the last one
+    // restores row_ptr[0] to 0.
+    const int64_t T = (R + kRowsPerTicket - 1) / kRowsPerTicket;
+    // With two rows per ticket, the first row of the pair in hand (the
+    // second is s_ticket's pair mate), kept in LDS so that no register holds
+    // it through the walk.
+    __shared__ int64_t s_next;
+    if (kRowsPerTicket > 1 && threadIdx.x == 0) s_next = R;
     for (int it = 0;; ++it) {
         if (threadIdx.x == 0) {
-            const int64_t t = (int64_t)atomicAdd(reinterpret_cast<unsigned long long*>(row_ptr), 1ull);
-            s_ticket = t;
-            // Every workgroup takes tickets until one is past the rows, so
-            // R + gridDim.x tickets are taken in all; the last one restores
-            // row_ptr[0] to 0.
-            if (t == R + (int64_t)gridDim.x - 1) status_store(row_ptr, 0);
+            if constexpr (kRowsPerTicket == 1) {
+                const int64_t t = (int64_t)atomicAdd(reinterpret_cast<unsigned long long*>(row_ptr), 1ull);
+                s_ticket = t;
+                if (t == T + (int64_t)gridDim.x - 1) status_store(row_ptr, 0);
+            } else if (s_next >= R) {
+                const int64_t t = (int64_t)atomicAdd(reinterpret_cast<unsigned long long*>(row_ptr), 1ull);
+                if (t == T + (int64_t)gridDim.x - 1) status_store(row_ptr, 0);
+                const int64_t first = t < T ? t * kRowsPerTicket : R;
+                s_ticket = first;
+                s_next = first + 1 < R ? first + 1 : R;
+            } else {
+                s_ticket = s_next;
+                s_next = R;
+            }
         }
         __syncthreads();   // also: the bitmap emitted last iteration is no longer read
         const int64_t r = uniform_i64(s_ticket);
@@ -736,10 +757,13 @@ size_t mask_smem_bytes(const MaskParams& p, int bitmaps = 1) {
 // Workgroups per CU below which a deeper one-pass pipeline costs more
 // occupancy than its shorter waits gain.
 constexpr int kMinResidentRows = 6;
+// Expected draws per row below which the one-pass build takes two rows per
+// ticket (measured crossover on MI355X between 4,900 and 6,600).
+constexpr int64_t kTicketPairDraws = 5000;
 
 template <int kDepth>
 hipError_t fused_occupancy(const MaskParams& p, int* blocks) {
-    return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks, k_mask_fused<kDepth>, kThreads,
+    return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks, k_mask_fused<kDepth, 1>, kThreads,
                                                         mask_smem_bytes(p, kDepth + 1));
 }
 
@@ -780,18 +804,31 @@ hipError_t launch_mask_fused(const MaskParams& p, int64_t* row_ptr, int32_t* col
             break;
         }
     }
+    // Rows per ticket.  One same-address atomic per row caps the build at a
+    // row per ~12.5 ns on MI355X whatever the row's work; light rows (expected
+    // draws per row, seeds x k at the middle row, below kTicketPairDraws)
+    // take two consecutive rows per ticket, which halves that floor.  Heavier
+    // rows keep one: a pair's second row publishes its size an iteration
+    // later, and the look-backs behind it wait (measured: 32k layer with 10
+    // seeds 0.84 -> 0.63 ms with pairs, 64k with 70 seeds 4.93 -> 5.47 ms).
+    const int64_t mid = p.q0 + p.nq / 2;
+    const int64_t work = (int64_t)p.n_seeds * row_count(p.ppm, p.causal ? mid + 1 : p.N);
+    const bool pairs = work < kTicketPairDraws;
+    const int64_t tickets = pairs ? (rows + 1) / 2 : rows;
     int64_t grid = (int64_t)(per_cu > 0 ? per_cu : 1) * (cus > 0 ? cus : 1);
-    if (grid > rows) grid = rows;
+    if (grid > tickets) grid = tickets;
     const size_t smem = mask_smem_bytes(p, depth + 1);
-    if (depth == 2)
-        hipLaunchKernelGGL(k_mask_fused<2>, dim3((unsigned)grid), dim3(kThreads), smem, st, p,
-                           row_ptr, col_idx, capacity);
-    else if (depth == 1)
-        hipLaunchKernelGGL(k_mask_fused<1>, dim3((unsigned)grid), dim3(kThreads), smem, st, p,
-                           row_ptr, col_idx, capacity);
-    else
-        hipLaunchKernelGGL(k_mask_fused<0>, dim3((unsigned)grid), dim3(kThreads), smem, st, p,
-                           row_ptr, col_idx, capacity);
+    const dim3 g3((unsigned)grid), b3(kThreads);
+    if (depth == 2) {
+        if (pairs) hipLaunchKernelGGL((k_mask_fused<2, 2>), g3, b3, smem, st, p, row_ptr, col_idx, capacity);
+        else hipLaunchKernelGGL((k_mask_fused<2, 1>), g3, b3, smem, st, p, row_ptr, col_idx, capacity);
+    } else if (depth == 1) {
+        if (pairs) hipLaunchKernelGGL((k_mask_fused<1, 2>), g3, b3, smem, st, p, row_ptr, col_idx, capacity);
+        else hipLaunchKernelGGL((k_mask_fused<1, 1>), g3, b3, smem, st, p, row_ptr, col_idx, capacity);
+    } else {
+        if (pairs) hipLaunchKernelGGL((k_mask_fused<0, 2>), g3, b3, smem, st, p, row_ptr, col_idx, capacity);
+        else hipLaunchKernelGGL((k_mask_fused<0, 1>), g3, b3, smem, st, p, row_ptr, col_idx, capacity);
+    }
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     const unsigned sb = (unsigned)((rows + 255) / 256);
