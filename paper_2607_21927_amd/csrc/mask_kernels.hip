@@ -617,9 +617,9 @@ __global__ __launch_bounds__(kThreads, kDepth == 2 ? 6 : 8) void k_mask_fused(Ma
     // past them, so T + gridDim.x tickets are taken in all, and the last one
     // restores row_ptr[0] to 0.
     const int64_t T = (R + kRowsPerTicket - 1) / kRowsPerTicket;
-    // With two rows per ticket, the first row of the pair in hand (the
-    // second is s_ticket's pair mate), kept in LDS so that no register holds
-    // it through the walk.
+    // With two rows per ticket, s_next holds the pair's second row until its
+    // turn (R when there is none); thread 0 alone uses it, and it lives in LDS
+    // so that no register holds it through the walk.
     __shared__ int64_t s_next;
     if (kRowsPerTicket > 1 && threadIdx.x == 0) s_next = R;
     for (int it = 0;; ++it) {
